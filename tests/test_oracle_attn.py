@@ -1,0 +1,295 @@
+"""Pins of the oracle's attention arithmetic (forward, backward, cache path).
+
+Each test names the property of arXiv 2408.00539 (or of the mathematics) it
+checks; none re-types the oracle's own formula.
+"""
+
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2408_00539_amd.workloads import segments_from_lengths, alternating
+
+
+def _rand(rng, *shape):
+    return rng.standard_normal(shape)
+
+
+def _random_layout(rng, n_dialogues, max_len, allow_any_flags=True):
+    dias = []
+    for _ in range(n_dialogues):
+        n = int(rng.integers(1, max_len + 1))
+        parts, left = [], n
+        while left:
+            ln = int(rng.integers(1, left + 1))
+            parts.append(ln)
+            left -= ln
+        if allow_any_flags:
+            flags = [bool(rng.integers(0, 2)) for _ in parts]
+        else:
+            flags = [i % 2 == 0 for i in range(len(parts))]
+        dias.append(list(zip(parts, flags)))
+    return segments_from_lengths(dias)
+
+
+def _fwd(q, k, v, segs, scale):
+    return oracle.fwd(q, k, v, segs.cu_seqlens, segs.cu_segs,
+                      segs.seg_is_query, scale)
+
+
+# ---------------------------------------------------------------- P-15
+
+@pytest.mark.parametrize("seed", range(6))
+def test_brute_force_matches_vectorised(seed):
+    """Per-element loops of Eq. 4 (softmax form) with Eq. 5 applied directly
+    must equal the vectorised oracle, including GQA and packed dialogues."""
+    rng = np.random.default_rng(seed)
+    segs = _random_layout(rng, int(rng.integers(1, 4)), 12)
+    hq, hkv = [(1, 1), (2, 1), (4, 2), (3, 3)][seed % 4]
+    d = 5
+    T = segs.total
+    q, k, v = _rand(rng, T, hq, d), _rand(rng, T, hkv, d), _rand(rng, T, hkv, d)
+    scale = 1 / math.sqrt(d)
+    o, lse = _fwd(q, k, v, segs, scale)
+    ob, lb = oracle.brute_force_fwd(q, k, v, segs.cu_seqlens, segs.cu_segs,
+                                    segs.seg_is_query, scale)
+    np.testing.assert_allclose(o, ob, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lb, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------- P-1/P-2/P-3 (library)
+
+def _sdpa(q, k, v, mask, scale):
+    torch = pytest.importorskip("torch")
+    qt = torch.from_numpy(q.transpose(1, 0, 2).copy())
+    kt = torch.from_numpy(k.transpose(1, 0, 2).copy())
+    vt = torch.from_numpy(v.transpose(1, 0, 2).copy())
+    out = torch.nn.functional.scaled_dot_product_attention(
+        qt, kt, vt, attn_mask=torch.from_numpy(mask), scale=scale)
+    return out.numpy().transpose(1, 0, 2)
+
+
+@pytest.mark.parametrize("kind", ["causal", "full", "prefix"])
+def test_special_cases_match_library_attention(kind):
+    """P-1 (Eq. 2), P-2 (Eq. 1), P-3 (Eq. 3) against torch's CPU fp64
+    scaled-dot-product attention with the textbook masks."""
+    rng = np.random.default_rng(11)
+    n, h, d = 37, 2, 16
+    q, k, v = _rand(rng, n, h, d), _rand(rng, n, h, d), _rand(rng, n, h, d)
+    scale = 1 / math.sqrt(d)
+    jj, ii = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    if kind == "causal":
+        segs = segments_from_lengths([[(10, False), (27, False)]])
+        mask = ii <= jj
+    elif kind == "full":
+        segs = segments_from_lengths([[(n, True)]])
+        mask = np.ones((n, n), dtype=bool)
+    else:
+        a = 13
+        segs = segments_from_lengths([[(a, True), (n - a, False)]])
+        mask = ii <= np.maximum(jj, a - 1)
+    o, _ = _fwd(q, k, v, segs, scale)
+    np.testing.assert_allclose(o, _sdpa(q, k, v, mask, scale), rtol=0,
+                               atol=1e-12)
+
+
+# ---------------------------------------------------------------- P-7
+
+@pytest.mark.parametrize("seed", range(3))
+def test_zero_query_closed_form(seed):
+    """Q = 0 makes the softmax uniform over the visible keys: O_j is the mean
+    of V over keys s_b..lim(j), and lse_j = ln(count)."""
+    rng = np.random.default_rng(100 + seed)
+    segs = _random_layout(rng, 3, 20)
+    T, d = segs.total, 4
+    q = np.zeros((T, 2, d))
+    k, v = _rand(rng, T, 1, d), _rand(rng, T, 1, d)
+    o, lse = _fwd(q, k, v, segs, 0.7)
+    # expected from the segment definition, token by token
+    for b in range(segs.batch):
+        s, e = segs.cu_seqlens[b], segs.cu_seqlens[b + 1]
+        for g in range(segs.num_segs):
+            a, c = segs.cu_segs[g], segs.cu_segs[g + 1]
+            if not (s <= a < e):
+                continue
+            for j in range(a, c):
+                last = c - 1 if segs.seg_is_query[g] else j
+                cnt = last - s + 1
+                for h in range(2):
+                    np.testing.assert_allclose(o[j, h], v[s:last + 1, 0].mean(0),
+                                               atol=1e-13)
+                    assert abs(lse[h, j] - math.log(cnt)) < 1e-13
+
+
+# ---------------------------------------------------------------- P-8
+
+def test_append_invariance():
+    """Sec. 2.1: no token attends past the end of its current query, so
+    appending later turns (or growing the last answer) leaves every earlier
+    row's output and LSE unchanged."""
+    rng = np.random.default_rng(7)
+    base = [5, 4, 3, 6, 2]           # Q A Q A Q
+    more = base + [7, 3, 4]           # ... A Q A appended
+    T2 = sum(more)
+    d = 8
+    q, k, v = _rand(rng, T2, 2, d), _rand(rng, T2, 2, d), _rand(rng, T2, 2, d)
+    s1 = segments_from_lengths([alternating(base)])
+    s2 = segments_from_lengths([alternating(more)])
+    T1 = s1.total
+    o1, l1 = _fwd(q[:T1], k[:T1], v[:T1], s1, 0.3)
+    o2, l2 = _fwd(q, k, v, s2, 0.3)
+    np.testing.assert_allclose(o2[:T1], o1, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(l2[:, :T1], l1, atol=1e-12, rtol=0)
+    # a later dialogue packed after it changes nothing either
+    s3 = segments_from_lengths([alternating(more), alternating([3, 3])])
+    T3 = s3.total
+    q3 = np.concatenate([q, _rand(rng, 6, 2, d)])
+    k3 = np.concatenate([k, _rand(rng, 6, 2, d)])
+    v3 = np.concatenate([v, _rand(rng, 6, 2, d)])
+    o3, l3 = _fwd(q3, k3, v3, s3, 0.3)
+    np.testing.assert_allclose(o3[:T2], o2, atol=1e-12, rtol=0)
+    assert T3 == T2 + 6
+
+
+# ---------------------------------------------------------------- P-9
+
+def test_permutation_within_query_segment():
+    """Eq. 4 sums over i <= f(j) without positions: permuting the tokens of
+    one query segment permutes that segment's outputs and, since every row
+    that sees one of them sees all of them, leaves all other rows unchanged."""
+    rng = np.random.default_rng(3)
+    lens = [4, 5, 6, 3, 4]           # Q A Q A Q
+    segs = segments_from_lengths([alternating(lens)])
+    T, d = segs.total, 6
+    q, k, v = _rand(rng, T, 1, d), _rand(rng, T, 1, d), _rand(rng, T, 1, d)
+    o, lse = _fwd(q, k, v, segs, 0.5)
+    a, c = 9, 15                     # the second query segment
+    perm = np.arange(T)
+    perm[a:c] = a + rng.permutation(c - a)
+    op, lp = _fwd(q[perm], k[perm], v[perm], segs, 0.5)
+    np.testing.assert_allclose(op, o[perm], atol=1e-12)
+    np.testing.assert_allclose(lp, lse[:, perm], atol=1e-12)
+
+
+# ---------------------------------------------------------------- P-10
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 1)])
+def test_stepwise_cache_equals_one_shot(hq, hkv):
+    """Sec. 2.3: reusing C_h, computing C_q, concatenating and generating the
+    answer token by token gives the rows of the one-shot forward over
+    [history; Q_n; A_n] with Q_n a query segment and A_n an answer segment."""
+    rng = np.random.default_rng(5)
+    hist = [6, 5, 3, 7]              # Q A Q A
+    Ln, steps, d = 5, 6, 8
+    lens = hist + [Ln, steps]
+    segs = segments_from_lengths([alternating(lens)])
+    T = segs.total
+    q, k, v = _rand(rng, T, hq, d), _rand(rng, T, hkv, d), _rand(rng, T, hkv, d)
+    o, lse = _fwd(q, k, v, segs, 0.4)
+    C = sum(hist)
+    on, ln_, kc, vc = oracle.prefill_cached(k[:C], v[:C], q[C:C + Ln],
+                                            k[C:C + Ln], v[C:C + Ln], 0.4)
+    np.testing.assert_allclose(on, o[C:C + Ln], atol=1e-12)
+    np.testing.assert_allclose(ln_, lse[:, C:C + Ln], atol=1e-12)
+    for t in range(steps):
+        p = C + Ln + t
+        ot, lt, kc, vc = oracle.decode_step(kc, vc, q[p], k[p], v[p], 0.4)
+        np.testing.assert_allclose(ot, o[p], atol=1e-12)
+        np.testing.assert_allclose(lt, lse[:, p], atol=1e-12)
+    assert kc.shape[0] == T
+
+
+# ------------------------------------------------------ P-11..P-13 backward
+
+def _loss_setup(seed, hq, hkv, d):
+    rng = np.random.default_rng(seed)
+    segs = segments_from_lengths([[(3, True), (2, False), (2, True)],
+                                  [(1, False), (3, True)]])
+    T = segs.total
+    q, k, v = _rand(rng, T, hq, d), _rand(rng, T, hkv, d), _rand(rng, T, hkv, d)
+    W = _rand(rng, T, hq, d)
+    return segs, q, k, v, W
+
+
+@pytest.mark.parametrize("hq,hkv", [(1, 1), (2, 1), (4, 2)])
+def test_gradients_central_differences(hq, hkv):
+    """P-11: dQ, dK, dV equal central finite differences of
+    loss = sum(O * W) (so dO = W), element by element."""
+    d, scale, h = 3, 0.6, 1e-6
+    segs, q, k, v, W = _loss_setup(1, hq, hkv, d)
+
+    def loss(q_, k_, v_):
+        o, _ = _fwd(q_, k_, v_, segs, scale)
+        return float(np.sum(o * W))
+
+    dq, dk, dv = oracle.bwd(q, k, v, W, segs.cu_seqlens, segs.cu_segs,
+                            segs.seg_is_query, scale)
+    for name, x, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        for idx in itertools.product(*[range(s) for s in x.shape]):
+            xp = x.copy()
+            xp[idx] += h
+            args = {"q": q, "k": k, "v": v}
+            args[name] = xp
+            up = loss(args["q"], args["k"], args["v"])
+            xp[idx] -= 2 * h
+            dn = loss(args["q"], args["k"], args["v"])
+            fd = (up - dn) / (2 * h)
+            assert abs(fd - g[idx]) <= 1e-7 * max(1.0, abs(fd)), (name, idx)
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 1)])
+def test_gradient_identities(hq, hkv):
+    """P-12: per dialogue and KV head the dK rows sum to zero (each row of
+    dS sums to zero by softmax shift invariance). P-13: the dV rows sum to
+    the dO rows summed over the dialogue and the head group (rows of P sum
+    to one)."""
+    rng = np.random.default_rng(9)
+    segs = _random_layout(rng, 3, 30, allow_any_flags=True)
+    T, d = segs.total, 7
+    q, k, v = _rand(rng, T, hq, d), _rand(rng, T, hkv, d), _rand(rng, T, hkv, d)
+    do = _rand(rng, T, hq, d)
+    dq, dk, dv = oracle.bwd(q, k, v, do, segs.cu_seqlens, segs.cu_segs,
+                            segs.seg_is_query, 0.5)
+    G = hq // hkv
+    for b in range(segs.batch):
+        s, e = segs.cu_seqlens[b], segs.cu_seqlens[b + 1]
+        for g in range(hkv):
+            np.testing.assert_allclose(dk[s:e, g].sum(0), 0, atol=1e-11)
+            np.testing.assert_allclose(
+                dv[s:e, g].sum(0), do[s:e, g * G:(g + 1) * G].sum((0, 1)),
+                atol=1e-11)
+
+
+def test_rowsum_identity_brute_force():
+    """P-14: sum_i P_ji dP_ji equals dO_j . O_j (loops on a tiny case), the
+    identity the GPU backward uses in place of the textbook D."""
+    rng = np.random.default_rng(4)
+    segs = segments_from_lengths([alternating([3, 2, 4])])
+    T, d = segs.total, 4
+    q, k, v, do = (_rand(rng, T, 1, d) for _ in range(4))
+    o, lse = _fwd(q, k, v, segs, 0.8)
+    L = oracle.lim(segs.cu_seqlens, segs.cu_segs, segs.seg_is_query)
+    for j in range(T):
+        keys = range(0, L[j] + 1)
+        p = [math.exp(0.8 * float(q[j, 0] @ k[i, 0]) - lse[0, j]) for i in keys]
+        dp = [float(do[j, 0] @ v[i, 0]) for i in keys]
+        lhs = sum(a * b for a, b in zip(p, dp))
+        assert abs(lhs - float(do[j, 0] @ o[j, 0])) < 1e-12
+
+
+def test_masked_keys_get_no_gradient_from_later_rows():
+    """With a causal (all-answer) dialogue the last key is seen only by the
+    last row, so its dK/dV come from that row alone (a mask-direction pin
+    for the backward)."""
+    rng = np.random.default_rng(2)
+    segs = segments_from_lengths([[(6, False)]])
+    T, d = 6, 4
+    q, k, v, do = (_rand(rng, T, 1, d) for _ in range(4))
+    dq, dk, dv = oracle.bwd(q, k, v, do, segs.cu_seqlens, segs.cu_segs,
+                            segs.seg_is_query, 1.0)
+    o, lse = _fwd(q, k, v, segs, 1.0)
+    p_last = math.exp(float(q[5, 0] @ k[5, 0]) - lse[0, 5])
+    np.testing.assert_allclose(dv[5, 0], p_last * do[5, 0], atol=1e-12)
