@@ -1,0 +1,167 @@
+/*
+ * ism_attn.h - C ABI of the MI355X (gfx950) ISM attention library.
+ *
+ * Intermittent Semi-working Mask (ISM) attention, arXiv 2408.00539.
+ * A packed batch holds several dialogues [P, Q_1, A_1, ..., Q_n, (A_n)]
+ * (Sec. 2.1, the sample definition before Eq. 4). By Eq. 5, a token of a query
+ * segment sees every earlier token of its dialogue and every token of its own
+ * query segment; a token of an answer segment sees the tokens up to and
+ * including itself. The attention itself is softmax(scale * Q K^T + M) V
+ * with that mask (Sec. 2.3: ISM changes only the causal mask of a standard
+ * decoder).
+ *
+ * Conventions shared by every entry point:
+ *  - Tensor pointers are DEVICE pointers owned by the caller. The library
+ *    allocates no memory and keeps no state between calls other than a
+ *    thread-local error string.
+ *  - bf16 tensors are passed as void* and are dense row-major:
+ *      q, o: [T, hq, d];  k, v: [T, hkv, d]   (T = tokens of the packed batch)
+ *      lse:  [hq, T] float32, natural-log log-sum-exp of the scaled scores.
+ *  - Grouped KV heads: query head h reads key/value head h / (hq / hkv);
+ *    hq must be a multiple of hkv. Supported head dims: d = 64 and d = 128.
+ *  - `scale` multiplies Q K^T before the softmax (normally 1/sqrt(d)).
+ *  - All work is enqueued on `stream` (a hipStream_t passed as void*, NULL =
+ *    the default stream). No call synchronises the device.
+ *  - `ws` is a caller-owned device workspace of at least
+ *    ism_attn_workspace_size(...) bytes, 256-byte aligned.
+ *  - On any error no kernel is launched, outputs are untouched, and a status
+ *    other than ISM_OK is returned; ism_last_error() gives the detail.
+ *    Faults of kernels already launched surface at the caller's next
+ *    synchronisation of the stream, as for any HIP kernel.
+ *  - Device-resident segment arrays are not inspected by the entry points
+ *    (that would need a synchronising copy); ism_check_segments_host()
+ *    validates a host copy of them.
+ *  - No entry point aborts, throws or exits the process.
+ */
+#ifndef ISM_ATTN_H
+#define ISM_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ISM_OK = 0,
+  ISM_ERR_NULL = 1,        /* a required pointer is NULL                    */
+  ISM_ERR_SHAPE = 2,       /* a size is out of range or inconsistent        */
+  ISM_ERR_UNSUPPORTED = 3, /* e.g. head dim other than 64 / 128             */
+  ISM_ERR_SEGMENTS = 4,    /* segment metadata violates its invariants      */
+  ISM_ERR_WORKSPACE = 5,   /* workspace missing, too small or misaligned    */
+  ISM_ERR_CAPACITY = 6,    /* KV cache capacity too small                   */
+  ISM_ERR_NO_DEVICE = 7,   /* no usable gfx950 device                       */
+  ISM_ERR_HIP = 8          /* a HIP runtime call or launch failed           */
+} ism_status;
+
+/* Dialogue structure of a packed batch (Sec. 2.1: the sample
+ * [P, Q_1, A_1, ..., Q_n] with boundaries m_p, m_{q_k}, m_{a_k}).
+ * Dialogue b covers tokens [cu_seqlens[b], cu_seqlens[b+1]); segment g covers
+ * [cu_segs[g], cu_segs[g+1]) and is a query segment (bidirectional block,
+ * Eq. 5 first two cases) iff seg_is_query[g] != 0, else an answer segment
+ * (causal, Eq. 5 third case). The prompt P is passed merged with Q_1 as one
+ * query segment (Eq. 5's first case covers both). Invariants: both arrays
+ * start at 0 and end at total_tokens, are strictly increasing (no empty
+ * segment or dialogue), and every cu_seqlens entry is also a cu_segs entry.
+ * max_seqlen must be >= the longest dialogue. Arrays live in device memory. */
+typedef struct {
+  const int32_t *cu_seqlens;   /* [batch + 1]    */
+  const int32_t *cu_segs;      /* [num_segs + 1] */
+  const uint8_t *seg_is_query; /* [num_segs]     */
+  int32_t batch;
+  int32_t num_segs;
+  int32_t total_tokens;
+  int32_t max_seqlen;
+} ism_segments;
+
+/* Workspace query. `op` is one of the ISM_OP_* values; unused arguments may
+ * be 0. Returns bytes (a multiple of 256), or 0 if none is needed. */
+enum { ISM_OP_FWD = 0, ISM_OP_BWD = 1, ISM_OP_PREFILL_CACHED = 2,
+       ISM_OP_DECODE = 3 };
+size_t ism_attn_workspace_size(int32_t op, int32_t batch, int32_t total_tokens,
+                               int32_t max_seqlen, int32_t hq, int32_t hkv,
+                               int32_t d, int32_t num_splits);
+
+/* Training / prefill forward over packed dialogues (Eq. 4 with the bound of
+ * Eq. 5, softmax form). Writes o [T, hq, d] bf16 and lse [hq, T] fp32
+ * (lse may be NULL). Workspace: ISM_OP_FWD. */
+ism_status ism_attn_fwd(const ism_segments *sg, const void *q, const void *k,
+                        const void *v, void *o, float *lse, int32_t hq,
+                        int32_t hkv, int32_t d, float scale, void *ws,
+                        size_t ws_bytes, void *stream);
+
+/* Backward of ism_attn_fwd (training on whole dialogues in one pass,
+ * Sec. 1 and Sec. 3.3). Inputs q, k, v, o, dout bf16 and lse fp32 as written
+ * by ism_attn_fwd on the same inputs. Outputs dq [T, hq, d], dk and dv
+ * [T, hkv, d] in fp32, overwritten. `deterministic` != 0 selects the
+ * reduction order that is bitwise repeatable from run to run.
+ * Workspace: ISM_OP_BWD. */
+ism_status ism_attn_bwd(const ism_segments *sg, const void *q, const void *k,
+                        const void *v, const void *o, const float *lse,
+                        const void *dout, float *dq, float *dk, float *dv,
+                        int32_t hq, int32_t hkv, int32_t d, float scale,
+                        int32_t deterministic, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* KV-cache reuse, new query segment (Sec. 2.3: reuse the history cache C_h,
+ * compute C_q, concatenate [C_h; C_q]). For dialogue b with C_b =
+ * cache_seqlens[b] cached tokens and L_b = cu_seqlens_new[b+1] -
+ * cu_seqlens_new[b] new tokens, the new keys/values are first written into
+ * the cache at positions [C_b, C_b + L_b); then every new row attends to all
+ * keys [0, C_b + L_b) (Eq. 5: f = m_{q_n} for the whole current query).
+ * q_new [Tn, hq, d], k_new / v_new [Tn, hkv, d] bf16 (Tn = total_new);
+ * k_cache / v_cache [batch, hkv, cache_cap, d] bf16, updated in place only in
+ * the append range; cache_seqlens [batch] device int32, read only (the
+ * caller advances it by L_b afterwards). o [Tn, hq, d] bf16, lse [hq, Tn]
+ * fp32 or NULL. The caller guarantees C_b + L_b <= cache_cap; max_new must
+ * be >= every L_b. Workspace: ISM_OP_PREFILL_CACHED. */
+ism_status ism_attn_prefill_cached(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
+    int32_t max_new, const void *q_new, const void *k_new, const void *v_new,
+    void *k_cache, void *v_cache, int32_t cache_cap,
+    const int32_t *cache_seqlens, void *o, float *lse, int32_t hq, int32_t hkv,
+    int32_t d, float scale, void *ws, size_t ws_bytes, void *stream);
+
+/* One answer-token decode step with the reused cache (Sec. 2.3, generation
+ * of A_n; Eq. 5 third case f(j) = j: the new token sees every cached token
+ * and itself). For dialogue b the new token sits at position
+ * p_b = cache_seqlens[b]: its key/value (k_new / v_new [batch, hkv, d]) are
+ * written into the cache at p_b, then q [batch, hq, d] attends to keys
+ * [0, p_b]. The key range is split into `num_splits` chunks processed in
+ * parallel and merged exactly (0 = choose automatically). o [batch, hq, d]
+ * bf16; lse [hq, batch] fp32 or NULL. The caller guarantees p_b < cache_cap
+ * and advances cache_seqlens by 1 afterwards. max_seqlen bounds p_b + 1 for
+ * the split choice (0 = cache_cap). Workspace: ISM_OP_DECODE with the same
+ * num_splits. */
+ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
+                           void *k_cache, void *v_cache, int32_t cache_cap,
+                           const int32_t *cache_seqlens, int32_t batch,
+                           int32_t max_seqlen, void *o, float *lse, int32_t hq,
+                           int32_t hkv, int32_t d, float scale,
+                           int32_t num_splits, void *ws, size_t ws_bytes,
+                           void *stream);
+
+/* Host-side validation of segment metadata (HOST pointers). Pure CPU, needs
+ * no device. Returns ISM_OK or ISM_ERR_SEGMENTS / ISM_ERR_NULL /
+ * ISM_ERR_SHAPE with the first violation in ism_last_error(). */
+ism_status ism_check_segments_host(const int32_t *cu_seqlens,
+                                   const int32_t *cu_segs,
+                                   const uint8_t *seg_is_query, int32_t batch,
+                                   int32_t num_segs, int32_t total_tokens,
+                                   int32_t max_seqlen);
+
+/* Static description of a status code. */
+const char *ism_status_string(ism_status s);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *ism_last_error(void);
+
+/* Library version, "major.minor.patch". */
+const char *ism_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISM_ATTN_H */

@@ -1,0 +1,279 @@
+// C ABI of the ISM attention library: argument checks, workspace layout and
+// the launch sequence of each entry point. Every check happens on the host
+// before any launch; nothing here synchronises the device.
+#include <math.h>
+#include <string.h>
+
+#include "../../include/ism_attn.h"
+#include "ism_host.h"
+#include "ism_kernels.h"
+
+namespace {
+
+using ism::fail;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Device check, cached per device ordinal: a gfx950 device must be current.
+ism_status check_device() {
+  static int ok_cache[64];  // 0 unknown, 1 ok, 2 bad
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) {
+    (void)hipGetLastError();
+    return fail(ISM_ERR_NO_DEVICE, "no HIP device visible");
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ISM_ERR_NO_DEVICE, "hipGetDevice failed");
+  }
+  if (dev >= 0 && dev < 64 && ok_cache[dev] == 1) return ISM_OK;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ISM_ERR_NO_DEVICE, "hipGetDeviceProperties failed");
+  }
+  const bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev >= 0 && dev < 64) ok_cache[dev] = ok ? 1 : 2;
+  if (!ok)
+    return fail(ISM_ERR_NO_DEVICE, "device %d is %s, library is built for gfx950",
+                dev, prop.gcnArchName);
+  return ISM_OK;
+}
+
+ism_status check_heads(int32_t hq, int32_t hkv, int32_t d, float scale) {
+  if (hq < 1 || hkv < 1 || hq % hkv != 0)
+    return fail(ISM_ERR_SHAPE, "need hq >= 1, hkv >= 1, hq %% hkv == 0 (hq=%d hkv=%d)",
+                hq, hkv);
+  if (d != 64 && d != 128)
+    return fail(ISM_ERR_UNSUPPORTED, "head dim %d not supported (64 or 128)", d);
+  if (!(scale > 0.f) || !isfinite(scale))
+    return fail(ISM_ERR_SHAPE, "scale must be finite and > 0 (got %g)", (double)scale);
+  return ISM_OK;
+}
+
+ism_status check_ws(const void *ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return ISM_OK;
+  if (!ws) return fail(ISM_ERR_WORKSPACE, "workspace of %zu bytes required", need);
+  if ((uintptr_t)ws % kAlign)
+    return fail(ISM_ERR_WORKSPACE, "workspace must be %zu-byte aligned", kAlign);
+  if (ws_bytes < need)
+    return fail(ISM_ERR_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+  return ISM_OK;
+}
+
+ism_status check_segments(const ism_segments *sg) {
+  if (!sg) return fail(ISM_ERR_NULL, "segments struct is NULL");
+  if (!sg->cu_seqlens || !sg->cu_segs || !sg->seg_is_query)
+    return fail(ISM_ERR_NULL, "segment array is NULL");
+  if (sg->batch < 1 || sg->num_segs < sg->batch || sg->total_tokens < sg->num_segs)
+    return fail(ISM_ERR_SHAPE,
+                "need batch >= 1, num_segs >= batch, total >= num_segs "
+                "(batch=%d num_segs=%d total=%d)",
+                sg->batch, sg->num_segs, sg->total_tokens);
+  if (sg->max_seqlen < 1 || sg->max_seqlen > sg->total_tokens)
+    return fail(ISM_ERR_SHAPE, "max_seqlen %d outside [1, total_tokens=%d]",
+                sg->max_seqlen, sg->total_tokens);
+  return ISM_OK;
+}
+
+ism_status hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return ISM_OK;
+  return fail(ISM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int decode_splits(int32_t batch, int32_t hkv, int32_t max_len, int32_t req) {
+  if (req > 0) return req;
+  const int slabs = batch * hkv;
+  int s = (4096 + slabs - 1) / slabs;
+  const int by_len = (max_len + 255) / 256;
+  if (s > by_len) s = by_len;
+  if (s > 64) s = 64;
+  return s < 1 ? 1 : s;
+}
+
+}  // namespace
+
+extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
+                                          int32_t total_tokens, int32_t max_seqlen,
+                                          int32_t hq, int32_t hkv, int32_t d,
+                                          int32_t num_splits) {
+  if (batch < 0 || total_tokens < 0 || hq < 0 || hkv < 0 || d < 0) return 0;
+  switch (op) {
+    case ISM_OP_FWD:
+      return align_up((size_t)total_tokens * 4);
+    case ISM_OP_BWD:
+      return align_up((size_t)total_tokens * 4) +
+             align_up((size_t)total_tokens * hq * 4);
+    case ISM_OP_PREFILL_CACHED:
+      return 0;
+    case ISM_OP_DECODE: {
+      if (hkv < 1) return 0;
+      const size_t s = (size_t)decode_splits(batch, hkv, max_seqlen, num_splits);
+      return align_up((size_t)batch * hq * s * d * 4) +
+             align_up((size_t)batch * hq * s * 2 * 4);
+    }
+  }
+  return 0;
+}
+
+extern "C" ism_status ism_attn_fwd(const ism_segments *sg, const void *q,
+                                   const void *k, const void *v, void *o,
+                                   float *lse, int32_t hq, int32_t hkv, int32_t d,
+                                   float scale, void *ws, size_t ws_bytes,
+                                   void *stream) {
+  ism::clear_error();
+  ism_status st = check_segments(sg);
+  if (st) return st;
+  if (!q || !k || !v || !o) return fail(ISM_ERR_NULL, "q, k, v and o are required");
+  if ((st = check_heads(hq, hkv, d, scale))) return st;
+  const size_t need = ism_attn_workspace_size(ISM_OP_FWD, sg->batch, sg->total_tokens,
+                                              sg->max_seqlen, hq, hkv, d, 0);
+  if ((st = check_ws(ws, ws_bytes, need))) return st;
+  if ((st = check_device())) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  int32_t *lim = (int32_t *)ws;
+  if ((st = hip_status(ism::launch_prep_lim(sg->cu_segs, sg->seg_is_query, sg->num_segs,
+                                            sg->total_tokens, lim, s),
+                       "prep launch")))
+    return st;
+  ism::FwdArgs a{};
+  a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
+  a.cu_q = sg->cu_seqlens;
+  a.lim = lim;
+  a.cache_len = nullptr;
+  a.batch = sg->batch; a.hq = hq; a.hkv = hkv;
+  a.total_q = sg->total_tokens;
+  a.max_rows = sg->max_seqlen;
+  a.kv_seq_stride = 0;
+  a.kv_head_stride = d;
+  a.kv_row_stride = (int64_t)hkv * d;
+  a.scale = scale;
+  return hip_status(ism::launch_fwd(a, d, false, s), "forward launch");
+}
+
+extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
+                                   const void *k, const void *v, const void *o,
+                                   const float *lse, const void *dout, float *dq,
+                                   float *dk, float *dv, int32_t hq, int32_t hkv,
+                                   int32_t d, float scale, int32_t deterministic,
+                                   void *ws, size_t ws_bytes, void *stream) {
+  ism::clear_error();
+  ism_status st = check_segments(sg);
+  if (st) return st;
+  if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv)
+    return fail(ISM_ERR_NULL, "q, k, v, o, lse, dout, dq, dk, dv are required");
+  if ((st = check_heads(hq, hkv, d, scale))) return st;
+  const size_t need = ism_attn_workspace_size(ISM_OP_BWD, sg->batch, sg->total_tokens,
+                                              sg->max_seqlen, hq, hkv, d, 0);
+  if ((st = check_ws(ws, ws_bytes, need))) return st;
+  if ((st = check_device())) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  int32_t *lim = (int32_t *)ws;
+  float *delta = (float *)((char *)ws + align_up((size_t)sg->total_tokens * 4));
+  if ((st = hip_status(ism::launch_prep_lim(sg->cu_segs, sg->seg_is_query, sg->num_segs,
+                                            sg->total_tokens, lim, s),
+                       "prep launch")))
+    return st;
+  ism::BwdArgs a{};
+  a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.delta = delta;
+  a.cu_seqlens = sg->cu_seqlens; a.cu_segs = sg->cu_segs;
+  a.seg_is_query = sg->seg_is_query; a.lim = lim;
+  a.batch = sg->batch; a.num_segs = sg->num_segs; a.hq = hq; a.hkv = hkv;
+  a.total = sg->total_tokens; a.max_seqlen = sg->max_seqlen;
+  a.scale = scale; a.deterministic = deterministic;
+  const hipError_t e = ism::launch_bwd(a, d, s);
+  if (e == hipErrorNotSupported)
+    return fail(ISM_ERR_UNSUPPORTED, "backward configuration not supported");
+  return hip_status(e, "backward launch");
+}
+
+extern "C" ism_status ism_attn_prefill_cached(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
+    const void *q_new, const void *k_new, const void *v_new, void *k_cache,
+    void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens, void *o,
+    float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+    size_t ws_bytes, void *stream) {
+  ism::clear_error();
+  if (!cu_seqlens_new || !q_new || !k_new || !v_new || !k_cache || !v_cache ||
+      !cache_seqlens || !o)
+    return fail(ISM_ERR_NULL, "a required pointer is NULL");
+  if (batch < 1 || total_new < 1 || max_new < 1 || max_new > total_new)
+    return fail(ISM_ERR_SHAPE,
+                "need batch >= 1, 1 <= max_new <= total_new (batch=%d total_new=%d "
+                "max_new=%d)", batch, total_new, max_new);
+  ism_status st = check_heads(hq, hkv, d, scale);
+  if (st) return st;
+  if (cache_cap < max_new)
+    return fail(ISM_ERR_CAPACITY, "cache_cap %d < max_new %d", cache_cap, max_new);
+  (void)ws; (void)ws_bytes;
+  if ((st = check_device())) return st;
+
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = hip_status(ism::launch_cache_append(k_new, v_new, k_cache, v_cache,
+                                                cu_seqlens_new, cache_seqlens, batch,
+                                                max_new, hkv, d, cache_cap, s),
+                       "cache append launch")))
+    return st;
+  ism::FwdArgs a{};
+  a.q = q_new; a.k = k_cache; a.v = v_cache; a.o = o; a.lse = lse;
+  a.cu_q = cu_seqlens_new;
+  a.lim = nullptr;
+  a.cache_len = cache_seqlens;
+  a.batch = batch; a.hq = hq; a.hkv = hkv;
+  a.total_q = total_new;
+  a.max_rows = max_new;
+  a.kv_seq_stride = (int64_t)hkv * cache_cap * d;
+  a.kv_head_stride = (int64_t)cache_cap * d;
+  a.kv_row_stride = d;
+  a.scale = scale;
+  return hip_status(ism::launch_fwd(a, d, true, s), "cached prefill launch");
+}
+
+extern "C" ism_status ism_attn_decode(const void *q, const void *k_new,
+                                      const void *v_new, void *k_cache,
+                                      void *v_cache, int32_t cache_cap,
+                                      const int32_t *cache_seqlens, int32_t batch,
+                                      int32_t max_seqlen, void *o, float *lse,
+                                      int32_t hq, int32_t hkv, int32_t d, float scale,
+                                      int32_t num_splits, void *ws, size_t ws_bytes,
+                                      void *stream) {
+  ism::clear_error();
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !cache_seqlens || !o)
+    return fail(ISM_ERR_NULL, "a required pointer is NULL");
+  if (batch < 1 || cache_cap < 1)
+    return fail(ISM_ERR_SHAPE, "need batch >= 1 and cache_cap >= 1");
+  ism_status st = check_heads(hq, hkv, d, scale);
+  if (st) return st;
+  const int g = hq / hkv;
+  if (g != 1 && g != 2 && g != 4 && g != 8)
+    return fail(ISM_ERR_UNSUPPORTED, "decode supports hq/hkv in {1,2,4,8} (got %d)", g);
+  if (max_seqlen == 0) max_seqlen = cache_cap;
+  if (max_seqlen < 1 || max_seqlen > cache_cap)
+    return fail(ISM_ERR_CAPACITY, "max_seqlen %d outside [1, cache_cap=%d]", max_seqlen,
+                cache_cap);
+  if (num_splits < 0 || num_splits > 1024)
+    return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
+  const int splits = decode_splits(batch, hkv, max_seqlen, num_splits);
+  const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen, hq,
+                                              hkv, d, num_splits);
+  if ((st = check_ws(ws, ws_bytes, need))) return st;
+  if ((st = check_device())) return st;
+
+  ism::DecodeArgs a{};
+  a.q = q; a.k_new = k_new; a.v_new = v_new;
+  a.k_cache = k_cache; a.v_cache = v_cache; a.pos = cache_seqlens;
+  a.o = o; a.lse = lse;
+  a.part_o = (float *)ws;
+  a.part_ml = (float *)((char *)ws + align_up((size_t)batch * hq * splits * d * 4));
+  a.batch = batch; a.hq = hq; a.hkv = hkv; a.cap = cache_cap;
+  a.splits = splits;
+  a.chunk = (max_seqlen + splits - 1) / splits;
+  a.scale = scale;
+  return hip_status(ism::launch_decode(a, d, (hipStream_t)stream), "decode launch");
+}

@@ -1,0 +1,261 @@
+// KV-cache reuse path of ISM attention on gfx950 (Sec. 2.3 of the paper):
+//  * cache append of a new query segment's keys/values (before the cached
+//    prefill, which then runs the forward kernel in cache mode);
+//  * one answer-token decode step: the token at position p sees keys
+//    [0, p] (Eq. 5 third case). The key range is split into chunks; each
+//    workgroup streams one chunk of one (dialogue, KV head) slab with 16-byte
+//    coalesced loads and keeps an unnormalised partial (m, l, o); a second
+//    kernel merges the partials exactly. The workgroup whose chunk holds p
+//    reads the new key/value from the input and also writes it into the
+//    cache, so no separate append launch is needed.
+//
+// Decode is a pure HBM stream (one query row per head: ~1 FLOP per byte), so
+// it uses VALU dot products, not MFMA.
+#include "ism_common.h"
+#include "ism_kernels.h"
+
+namespace ism {
+
+namespace {
+
+__global__ void __launch_bounds__(256)
+cache_append_kernel(const bf16_t *__restrict__ k_src,
+                    const bf16_t *__restrict__ v_src, bf16_t *__restrict__ k_cache,
+                    bf16_t *__restrict__ v_cache, const int32_t *__restrict__ cu_new,
+                    const int32_t *__restrict__ cache_len, int32_t hkv, int32_t d,
+                    int32_t cap) {
+  const int b = blockIdx.y;
+  const int r0 = cu_new[b], n = cu_new[b + 1] - r0;
+  const int cpr = hkv * (d / 8);  // 16-byte chunks per source row
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * cpr) return;
+  const int r = (int)(idx / cpr), rem = (int)(idx % cpr);
+  const int pos = cache_len[b] + r;
+  if (pos < 0 || pos >= cap) return;  // out of contract: never write outside the slab
+  const int h = rem / (d / 8), c = rem % (d / 8);
+  const int64_t src = ((int64_t)(r0 + r) * hkv + h) * d + c * 8;
+  const int64_t dst = (((int64_t)b * hkv + h) * cap + pos) * d + c * 8;
+  *(u32x4 *)(k_cache + dst) = *(const u32x4 *)(k_src + src);
+  *(u32x4 *)(v_cache + dst) = *(const u32x4 *)(v_src + src);
+}
+
+template <int D, int G>
+__global__ void __launch_bounds__(256)
+decode_split_kernel(DecodeArgs a) {
+  constexpr int CPK = D / 8;     // lanes per key row (16 bytes each)
+  constexpr int KPI = 64 / CPK;  // keys per wave-wide load
+  constexpr int U = 8;           // loads in flight per lane per tensor
+  constexpr int KPW = U * KPI;   // keys per wave per iteration
+  __shared__ float sm_o[4][G][D];
+  __shared__ float sm_m[4][G], sm_l[4][G];
+
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane % CPK, slot = lane / CPK;
+  // position of the new token; clamped so that out-of-contract positions
+  // never address memory outside the slab
+  const int p = min(max(a.pos[b], 0), a.cap - 1);
+  // the last chunk runs to p even if the host's bound on p was too small
+  const int k0 = split * a.chunk;
+  const int k1 = split == a.splits - 1 ? p + 1 : min(k0 + a.chunk, p + 1);
+  const int owner = min(p / a.chunk, a.splits - 1);
+  const float sl2 = a.scale * kLog2e;
+
+  const int64_t slab = ((int64_t)b * a.hkv + kvh) * a.cap * D;
+  const bf16_t *kc = (const bf16_t *)a.k_cache + slab + c * 8;
+  const bf16_t *vc = (const bf16_t *)a.v_cache + slab + c * 8;
+  const bf16_t *kn = (const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
+  const bf16_t *vn = (const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
+
+  if (split == owner && tid < CPK) {
+    // this chunk owns the new token: store it into the cache
+    *(u32x4 *)((bf16_t *)a.k_cache + slab + (int64_t)p * D + tid * 8) =
+        *(const u32x4 *)((const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
+    *(u32x4 *)((bf16_t *)a.v_cache + slab + (int64_t)p * D + tid * 8) =
+        *(const u32x4 *)((const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
+  }
+
+  float qv[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const u32x4 w = *(const u32x4 *)((const bf16_t *)a.q +
+                                     ((int64_t)b * a.hq + kvh * G + g) * D + c * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      qv[g][2 * i] = bf16_lo(w[i]) * sl2;
+      qv[g][2 * i + 1] = bf16_hi(w[i]) * sl2;
+    }
+  }
+  float m[G], l[G], o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[g][i] = 0.f;
+  }
+
+  for (int base = k0 + wave * KPW; base < k1; base += 4 * KPW) {
+    u32x4 kr[U], vr[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int key = min(base + u * KPI + slot, p);
+      const bool isnew = key == p;
+      kr[u] = *(const u32x4 *)(isnew ? kn : kc + (int64_t)key * D);
+      vr[u] = *(const u32x4 *)(isnew ? vn : vc + (int64_t)key * D);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float s[U];
+      float mt = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc = fmaf(qv[g][2 * i], bf16_lo(kr[u][i]), acc);
+          acc = fmaf(qv[g][2 * i + 1], bf16_hi(kr[u][i]), acc);
+        }
+#pragma unroll
+        for (int x = 1; x < CPK; x <<= 1) acc += __shfl_xor(acc, x);
+        s[u] = (base + u * KPI + slot < k1) ? acc : -INFINITY;
+        mt = fmaxf(mt, s[u]);
+      }
+      const float mnew = fmaxf(m[g], mt);
+      const float mref = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = fast_exp2(m[g] - mref);
+      m[g] = mnew;
+      l[g] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[g][i] *= alpha;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float pu = fast_exp2(s[u] - mref);
+        l[g] += pu;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          o[g][2 * i] = fmaf(pu, bf16_lo(vr[u][i]), o[g][2 * i]);
+          o[g][2 * i + 1] = fmaf(pu, bf16_hi(vr[u][i]), o[g][2 * i + 1]);
+        }
+      }
+    }
+  }
+
+  // merge the key slots of the wave (lanes with equal c), then the 4 waves
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int x = CPK; x < 64; x <<= 1) {
+      const float m2 = __shfl_xor(m[g], x);
+      const float l2 = __shfl_xor(l[g], x);
+      const float mn = fmaxf(m[g], m2);
+      const float mref = mn == -INFINITY ? 0.f : mn;
+      const float f1 = fast_exp2(m[g] - mref), f2 = fast_exp2(m2 - mref);
+      l[g] = l[g] * f1 + l2 * f2;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float o2 = __shfl_xor(o[g][i], x);
+        o[g][i] = o[g][i] * f1 + o2 * f2;
+      }
+      m[g] = mn;
+    }
+    if (slot == 0) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sm_o[wave][g][c * 8 + i] = o[g][i];
+      if (c == 0) { sm_m[wave][g] = m[g]; sm_l[wave][g] = l[g]; }
+    }
+  }
+  __syncthreads();
+  for (int t = tid; t < G * D; t += 256) {
+    const int g = t / D, dd = t % D;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, sm_m[w][g]);
+    const float mref = mx == -INFINITY ? 0.f : mx;
+    float lt = 0.f, ot = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = fast_exp2(sm_m[w][g] - mref);
+      lt += sm_l[w][g] * f;
+      ot += sm_o[w][g][dd] * f;
+    }
+    const int h = kvh * G + g;
+    const int64_t pi = ((int64_t)b * a.hq + h) * a.splits + split;
+    a.part_o[pi * D + dd] = ot;
+    if (dd == 0) {
+      a.part_ml[pi * 2] = mx;
+      a.part_ml[pi * 2 + 1] = lt;
+    }
+  }
+}
+
+// Exact merge of the split partials: M = max m_s, L = sum l_s 2^(m_s - M),
+// O = sum o_s 2^(m_s - M) / L. Scores were kept in log2 units.
+template <int D>
+__global__ void __launch_bounds__(D)
+decode_combine_kernel(DecodeArgs a) {
+  const int bh = blockIdx.x;  // b * hq + h
+  const int dd = threadIdx.x;
+  const float *ml = a.part_ml + (int64_t)bh * a.splits * 2;
+  float mx = -INFINITY;
+  for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, ml[2 * s]);
+  const float mref = mx == -INFINITY ? 0.f : mx;
+  float lt = 0.f, ot = 0.f;
+  const float *po = a.part_o + (int64_t)bh * a.splits * D + dd;
+  for (int s = 0; s < a.splits; ++s) {
+    const float f = fast_exp2(ml[2 * s] - mref);
+    lt += ml[2 * s + 1] * f;
+    ot += po[(int64_t)s * D] * f;
+  }
+  ((bf16_t *)a.o)[(int64_t)bh * D + dd] = (bf16_t)(ot / lt);
+  if (a.lse && dd == 0) {
+    const int b = bh / a.hq, h = bh % a.hq;
+    a.lse[(int64_t)h * a.batch + b] = (mx + log2f(lt)) * kLn2;
+  }
+}
+
+template <int D, int G>
+hipError_t launch_decode_t(const DecodeArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL((decode_split_kernel<D, G>),
+                     dim3(a.splits, a.hkv, a.batch), dim3(256), 0, stream, a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(a.batch * a.hq), dim3(D),
+                     0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
+  switch (a.hq / a.hkv) {
+    case 1: return launch_decode_t<D, 1>(a, stream);
+    case 2: return launch_decode_t<D, 2>(a, stream);
+    case 4: return launch_decode_t<D, 4>(a, stream);
+    case 8: return launch_decode_t<D, 8>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_cache_append(const void *k_src, const void *v_src,
+                               void *k_cache, void *v_cache,
+                               const int32_t *cu_new, const int32_t *cache_len,
+                               int32_t batch, int32_t max_new, int32_t hkv,
+                               int32_t d, int32_t cap, hipStream_t stream) {
+  const int64_t chunks = (int64_t)max_new * hkv * (d / 8);
+  if (chunks == 0 || batch == 0) return hipSuccess;
+  hipLaunchKernelGGL(cache_append_kernel, dim3((unsigned)((chunks + 255) / 256), batch),
+                     dim3(256), 0, stream, (const bf16_t *)k_src,
+                     (const bf16_t *)v_src, (bf16_t *)k_cache, (bf16_t *)v_cache,
+                     cu_new, cache_len, hkv, d, cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream) {
+  if (d == 128) return launch_decode_d<128>(a, stream);
+  if (d == 64) return launch_decode_d<64>(a, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ism

@@ -1,0 +1,84 @@
+// Internal launch interface between the C ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ism {
+
+// Forward attention over row tiles. Two modes share one kernel:
+//  * packed (training / prefill): rows and keys live on the packed token axis,
+//    key i of dialogue b is row i of k/v (stride hkv*d), and row j sees keys
+//    [cu_q[b], lim[j]];
+//  * cache (KV reuse): rows are the new query tokens of dialogue b, keys are
+//    rows 0..C_b+L_b-1 of that dialogue's cache slab, all visible.
+struct FwdArgs {
+  const void *q;
+  const void *k;
+  const void *v;
+  void *o;
+  float *lse;               // may be null
+  const int32_t *cu_q;      // [batch+1] row ranges of q / o
+  const int32_t *lim;       // packed mode: [T] inclusive key bound per row
+  const int32_t *cache_len; // cache mode: [batch] cached tokens C_b
+  int32_t batch;
+  int32_t hq;
+  int32_t hkv;
+  int32_t total_q;          // rows of q (T or Tn)
+  int32_t max_rows;         // longest row range of a dialogue
+  int64_t kv_seq_stride;    // elements between dialogues' K/V (cache mode)
+  int64_t kv_head_stride;   // elements between KV heads
+  int64_t kv_row_stride;    // elements between consecutive keys
+  float scale;
+};
+
+hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
+                           int32_t num_segs, int32_t total, int32_t *lim,
+                           hipStream_t stream);
+
+hipError_t launch_fwd(const FwdArgs &a, int d, bool cache_mode,
+                      hipStream_t stream);
+
+// Cache append: rows [cu_new[b], cu_new[b+1]) of src go to positions
+// cache_len[b] + (r - cu_new[b]) of slab b. src is [Tn, hkv, d];
+// cache is [batch, hkv, cap, d].
+hipError_t launch_cache_append(const void *k_src, const void *v_src,
+                               void *k_cache, void *v_cache,
+                               const int32_t *cu_new, const int32_t *cache_len,
+                               int32_t batch, int32_t max_new, int32_t hkv,
+                               int32_t d, int32_t cap, hipStream_t stream);
+
+struct DecodeArgs {
+  const void *q;            // [batch, hq, d]
+  const void *k_new;        // [batch, hkv, d]
+  const void *v_new;
+  void *k_cache;            // [batch, hkv, cap, d]
+  void *v_cache;
+  const int32_t *pos;       // [batch] position of the new token
+  void *o;                  // [batch, hq, d]
+  float *lse;               // [hq, batch] or null
+  float *part_o;            // [batch, hq, splits, d]
+  float *part_ml;           // [batch, hq, splits, 2]
+  int32_t batch, hq, hkv, cap, splits, chunk;
+  float scale;
+};
+
+hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream);
+
+struct BwdArgs {
+  const void *q, *k, *v, *o, *dout;
+  const float *lse;
+  float *dq, *dk, *dv;
+  float *delta;             // [hq, T] workspace: rowsum(dO * O)
+  const int32_t *cu_seqlens;
+  const int32_t *cu_segs;
+  const uint8_t *seg_is_query;
+  const int32_t *lim;       // [T]
+  int32_t batch, num_segs, hq, hkv, total, max_seqlen;
+  float scale;
+  int32_t deterministic;
+};
+
+hipError_t launch_bwd(const BwdArgs &a, int d, hipStream_t stream);
+
+}  // namespace ism

@@ -1,0 +1,281 @@
+"""Python binding of libism_attn.so (ctypes; argument marshalling only).
+
+Every function takes torch tensors already on the GPU, allocates the outputs
+and the workspace with torch, passes raw pointers and torch's current HIP
+stream to the C ABI, and raises on any status other than ISM_OK. There is no
+fallback: if the library is not built or no gfx950 device is present, the
+call fails loudly.
+
+Names follow the C ABI (include/ism_attn.h): fwd, bwd, prefill_cached,
+decode, plus check_segments_host and workspace_size.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libism_attn.so")
+
+ISM_OP_FWD, ISM_OP_BWD, ISM_OP_PREFILL_CACHED, ISM_OP_DECODE = range(4)
+STATUS = {0: "ISM_OK", 1: "ISM_ERR_NULL", 2: "ISM_ERR_SHAPE",
+          3: "ISM_ERR_UNSUPPORTED", 4: "ISM_ERR_SEGMENTS",
+          5: "ISM_ERR_WORKSPACE", 6: "ISM_ERR_CAPACITY",
+          7: "ISM_ERR_NO_DEVICE", 8: "ISM_ERR_HIP"}
+
+
+class IsmError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class ism_segments(ctypes.Structure):
+    _fields_ = [("cu_seqlens", ctypes.c_void_p),
+                ("cu_segs", ctypes.c_void_p),
+                ("seg_is_query", ctypes.c_void_p),
+                ("batch", ctypes.c_int32),
+                ("num_segs", ctypes.c_int32),
+                ("total_tokens", ctypes.c_int32),
+                ("max_seqlen", ctypes.c_int32)]
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_F = ctypes.c_float
+_Z = ctypes.c_size_t
+
+_SIGS = {
+    "ism_attn_workspace_size": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I]),
+    "ism_attn_fwd": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P, _P, _P,
+                          _I, _I, _I, _F, _P, _Z, _P]),
+    "ism_attn_bwd": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P, _P, _P,
+                          _P, _P, _P, _P, _I, _I, _I, _F, _I, _P, _Z, _P]),
+    "ism_attn_prefill_cached": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _I,
+                                     _P, _P, _P, _I, _I, _I, _F, _P, _Z, _P]),
+    "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
+                             _I, _I, _F, _I, _P, _Z, _P]),
+    "ism_check_segments_host": (_I, [_P, _P, _P, _I, _I, _I, _I]),
+    "ism_status_string": (ctypes.c_char_p, [_I]),
+    "ism_last_error": (ctypes.c_char_p, []),
+    "ism_version": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+def lib():
+    """Load the library once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2408_00539_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != 0:
+        raise IsmError(status, lib().ism_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t, name, dtype, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+
+
+def workspace_size(op, batch=0, total_tokens=0, max_seqlen=0, hq=0, hkv=0,
+                   d=0, num_splits=0):
+    return int(lib().ism_attn_workspace_size(op, batch, total_tokens,
+                                             max_seqlen, hq, hkv, d,
+                                             num_splits))
+
+
+def _workspace(nbytes, device):
+    torch = _torch()
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+class Segments:
+    """Device-resident dialogue structure of a packed batch.
+
+    cu_seqlens [B+1] int32, cu_segs [S+1] int32, seg_is_query [S] uint8,
+    plus host scalars. ``from_host`` uploads numpy arrays.
+    """
+
+    def __init__(self, cu_seqlens, cu_segs, seg_is_query, total_tokens,
+                 max_seqlen):
+        torch = _torch()
+        _need(cu_seqlens, "cu_seqlens", torch.int32)
+        _need(cu_segs, "cu_segs", torch.int32)
+        _need(seg_is_query, "seg_is_query", torch.uint8)
+        self.cu_seqlens, self.cu_segs, self.seg_is_query = (
+            cu_seqlens, cu_segs, seg_is_query)
+        self.batch = cu_seqlens.numel() - 1
+        self.num_segs = seg_is_query.numel()
+        self.total_tokens = int(total_tokens)
+        self.max_seqlen = int(max_seqlen)
+
+    @classmethod
+    def from_host(cls, cu_seqlens, cu_segs, seg_is_query, device="cuda"):
+        import numpy as np
+        torch = _torch()
+        cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+        return cls(torch.from_numpy(cu).to(device),
+                   torch.from_numpy(np.ascontiguousarray(cu_segs, np.int32)).to(device),
+                   torch.from_numpy(np.ascontiguousarray(seg_is_query, np.uint8)).to(device),
+                   int(cu[-1]), int(np.max(np.diff(cu))))
+
+    def c_struct(self):
+        return ism_segments(self.cu_seqlens.data_ptr(), self.cu_segs.data_ptr(),
+                            self.seg_is_query.data_ptr(), self.batch,
+                            self.num_segs, self.total_tokens, self.max_seqlen)
+
+
+def fwd(q, k, v, segs, scale=None, return_lse=True):
+    """ISM forward over packed dialogues. q [T,hq,d], k/v [T,hkv,d] bf16.
+    Returns (o bf16 [T,hq,d], lse fp32 [hq,T] or None)."""
+    torch = _torch()
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    _need(q, "q", torch.bfloat16)
+    _need(k, "k", torch.bfloat16, (T, hkv, d))
+    _need(v, "v", torch.bfloat16, (T, hkv, d))
+    if T != segs.total_tokens:
+        raise ValueError("q rows != segs.total_tokens")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, T), dtype=torch.float32, device=q.device) \
+        if return_lse else None
+    nws = workspace_size(ISM_OP_FWD, segs.batch, T, segs.max_seqlen, hq, hkv, d)
+    ws = _workspace(nws, q.device)
+    sg = segs.c_struct()
+    _check(lib().ism_attn_fwd(ctypes.byref(sg), _ptr(q), _ptr(k), _ptr(v),
+                              _ptr(o), _ptr(lse), hq, hkv, d, scale, _ptr(ws),
+                              nws, _stream()))
+    return o, lse
+
+
+def bwd(q, k, v, o, lse, dout, segs, scale=None, deterministic=False):
+    """Gradients (dq [T,hq,d], dk, dv [T,hkv,d], fp32) of ism fwd."""
+    torch = _torch()
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
+        _need(t, n, torch.bfloat16)
+    _need(lse, "lse", torch.float32, (hq, T))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
+    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    nws = workspace_size(ISM_OP_BWD, segs.batch, T, segs.max_seqlen, hq, hkv, d)
+    ws = _workspace(nws, q.device)
+    sg = segs.c_struct()
+    _check(lib().ism_attn_bwd(ctypes.byref(sg), _ptr(q), _ptr(k), _ptr(v),
+                              _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq),
+                              _ptr(dk), _ptr(dv), hq, hkv, d, scale,
+                              1 if deterministic else 0, _ptr(ws), nws,
+                              _stream()))
+    return dq, dk, dv
+
+
+def prefill_cached(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
+                   cu_seqlens_new, max_new, scale=None, return_lse=True):
+    """New query segment against the reused cache (appends k_new/v_new).
+    Returns (o [Tn,hq,d] bf16, lse [hq,Tn] fp32 or None)."""
+    torch = _torch()
+    Tn, hq, d = q_new.shape
+    B, hkv, cap, _ = k_cache.shape
+    _need(q_new, "q_new", torch.bfloat16)
+    _need(k_new, "k_new", torch.bfloat16, (Tn, hkv, d))
+    _need(v_new, "v_new", torch.bfloat16, (Tn, hkv, d))
+    _need(k_cache, "k_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(v_cache, "v_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
+    _need(cu_seqlens_new, "cu_seqlens_new", torch.int32, (B + 1,))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q_new)
+    lse = torch.empty((hq, Tn), dtype=torch.float32, device=q_new.device) \
+        if return_lse else None
+    _check(lib().ism_attn_prefill_cached(
+        _ptr(cu_seqlens_new), B, Tn, int(max_new), _ptr(q_new), _ptr(k_new),
+        _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap, _ptr(cache_seqlens),
+        _ptr(o), _ptr(lse), hq, hkv, d, scale, None, 0, _stream()))
+    return o, lse
+
+
+def decode(q, k_new, v_new, k_cache, v_cache, cache_seqlens, max_seqlen=0,
+           scale=None, num_splits=0, return_lse=True, workspace=None):
+    """One decode step (appends k_new/v_new at cache_seqlens[b]).
+    Returns (o [B,hq,d] bf16, lse [hq,B] fp32 or None)."""
+    torch = _torch()
+    B, hq, d = q.shape
+    _, hkv, cap, _ = k_cache.shape
+    _need(q, "q", torch.bfloat16)
+    _need(k_new, "k_new", torch.bfloat16, (B, hkv, d))
+    _need(v_new, "v_new", torch.bfloat16, (B, hkv, d))
+    _need(k_cache, "k_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(v_cache, "v_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ms = cap if not max_seqlen else int(max_seqlen)
+    nws = workspace_size(ISM_OP_DECODE, B, 0, ms, hq, hkv, d, num_splits)
+    ws = workspace if workspace is not None else _workspace(nws, q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, B), dtype=torch.float32, device=q.device) \
+        if return_lse else None
+    _check(lib().ism_attn_decode(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap,
+        _ptr(cache_seqlens), B, ms, _ptr(o), _ptr(lse), hq, hkv, d, scale,
+        int(num_splits), _ptr(ws), nws if workspace is None else
+        workspace.numel(), _stream()))
+    return o, lse
+
+
+def check_segments_host(cu_seqlens, cu_segs, seg_is_query, max_seqlen=None):
+    """Validate host (numpy) segment arrays with the library's checker.
+    Returns (status, detail)."""
+    import numpy as np
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    cs = np.ascontiguousarray(cu_segs, dtype=np.int32)
+    fl = np.ascontiguousarray(seg_is_query, dtype=np.uint8)
+    ms = int(np.max(np.diff(cu))) if max_seqlen is None and len(cu) > 1 \
+        else int(max_seqlen or 0)
+    st = lib().ism_check_segments_host(
+        cu.ctypes.data, cs.ctypes.data, fl.ctypes.data, len(cu) - 1, len(fl),
+        int(cu[-1]) if len(cu) else 0, ms)
+    return st, lib().ism_last_error().decode()
