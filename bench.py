@@ -1,0 +1,332 @@
+"""Benchmark of the ISM attention hot path on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                [--only step|all]
+
+A step is one training pass of the attention hot path over one batch of
+workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
+visibility prep, the forward and, once built, the backward. ``value`` is the
+useful (unmasked) TFLOP/s of that step: 4*d FLOPs per visible (row, key) pair
+and query head for the forward, 10*d for the backward. The other paths of the
+hot path are measured on their own workloads and reported under ``paths``:
+the grouped-KV forward (workload 2), the cached prefill and the decode stream
+(workload 3), the backward (workload 4).
+
+The last line of stdout is one JSON object; everything else goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("ISM attention useful TFLOP/s (fwd, bwd) and % bf16 MFMA peak; "
+          "decode HBM GB/s")
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def visible_pairs(segs):
+    """Useful (row, key) pairs per query head under the ISM bound: a row of a
+    query segment [a, c) sees c - s_b keys, an answer row j sees j - s_b + 1."""
+    tot = 0
+    cu, cs, fl = segs.cu_seqlens, segs.cu_segs, segs.seg_is_query
+    b = 0
+    for g in range(len(fl)):
+        a, c = int(cs[g]), int(cs[g + 1])
+        while not (cu[b] <= a < cu[b + 1]):
+            b += 1
+        s = int(cu[b])
+        n = c - a
+        if fl[g]:
+            tot += n * (c - s)
+        else:
+            tot += (a - s + 1 + c - s) * n // 2
+    return tot
+
+
+def dev(bits):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.bfloat16).to("cuda")
+
+
+class Timer:
+    """HIP-event timing on torch's current stream (where the ops launch)."""
+
+    def __init__(self):
+        import torch
+        self.torch = torch
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def run(self, fn, reps, warmup):
+        for _ in range(warmup):
+            fn()
+        self.torch.cuda.synchronize()
+        self.a.record()
+        for _ in range(reps):
+            fn()
+        self.b.record()
+        self.torch.cuda.synchronize()
+        return self.a.elapsed_time(self.b) / reps
+
+
+def bench_training(w, timer, steps, warmup, with_bwd):
+    from paper_2408_00539_amd import ops
+    import torch
+    segs = ops.Segments.from_host(w.segs.cu_seqlens, w.segs.cu_segs,
+                                  w.segs.seg_is_query)
+    q, k, v = dev(w.q), dev(w.k), dev(w.v)
+    pairs = visible_pairs(w.segs)
+    f_fwd = 4 * w.d * w.hq * pairs
+    f_bwd = 10 * w.d * w.hq * pairs
+    res = {"visible_pairs_per_head": pairs}
+    o, lse = ops.fwd(q, k, v, segs, w.scale)
+    ms_fwd = timer.run(lambda: ops.fwd(q, k, v, segs, w.scale), steps, warmup)
+    res["fwd"] = {"ms": ms_fwd, "tflops": f_fwd / ms_fwd / 1e9,
+                  "frac_peak": f_fwd / ms_fwd / 1e9 / PEAK_BF16_TFLOPS,
+                  "flop": f_fwd}
+    if with_bwd:
+        do = dev(w.do) if w.do is not None else torch.randn_like(q)
+        ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale),
+                           steps, warmup)
+        res["bwd"] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
+                      "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
+                      "flop": f_bwd}
+
+        def step():
+            o2, l2 = ops.fwd(q, k, v, segs, w.scale)
+            ops.bwd(q, k, v, o2, l2, do, segs, w.scale)
+        ms_step = timer.run(step, steps, warmup)
+        res["step"] = {"ms": ms_step, "flop": f_fwd + f_bwd}
+    else:
+        res["step"] = {"ms": ms_fwd, "flop": f_fwd}
+    return res
+
+
+def bench_cache(w, timer, reps, warmup):
+    from paper_2408_00539_amd import ops
+    import torch
+    B = len(w.new_lens)
+    Kc, Vc = dev(w.k_cache), dev(w.v_cache)
+    lens = torch.full((B,), w.hist_len, dtype=torch.int32, device="cuda")
+    cu = torch.from_numpy(w.cu_new).cuda()
+    qn, kn, vn = dev(w.q_new), dev(w.k_new), dev(w.v_new)
+    mx = int(w.new_lens.max())
+    L = w.new_lens.astype(np.int64)
+    ms_pf = timer.run(lambda: ops.prefill_cached(qn, kn, vn, Kc, Vc, lens, cu,
+                                                 mx, w.scale), reps, warmup)
+    f_pf = 4 * w.d * w.hq * float(np.sum(L * (w.hist_len + L)))
+    b_pf = 2 * w.hkv * w.d * 2 * float(np.sum(w.hist_len + L))
+    out = {"prefill_cached": {
+        "ms": ms_pf, "tflops": f_pf / ms_pf / 1e9,
+        "frac_peak_mfma": f_pf / ms_pf / 1e9 / PEAK_BF16_TFLOPS,
+        "kv_gbs": b_pf / ms_pf / 1e6,
+        "bound_ms": max(f_pf / PEAK_BF16_TFLOPS / 1e9, b_pf / PEAK_HBM_GBS / 1e6),
+        "flop": f_pf, "kv_bytes": b_pf}}
+    out["prefill_cached"]["frac_of_bound"] = out["prefill_cached"]["bound_ms"] / ms_pf
+
+    qd, kd, vd = dev(w.q_dec), dev(w.k_dec), dev(w.v_dec)
+    pos0 = lens + torch.from_numpy(w.new_lens).cuda()
+    ws = torch.empty(ops.workspace_size(ops.ISM_OP_DECODE, B, 0, w.cache_cap,
+                                        w.hq, w.hkv, w.d, 0),
+                     dtype=torch.uint8, device="cuda")
+
+    def turn():
+        pos = pos0.clone()
+        for t in range(w.steps):
+            ops.decode(qd[t], kd[t], vd[t], Kc, Vc, pos, 0, w.scale,
+                       workspace=ws)
+            pos += 1
+    ms_turn = timer.run(turn, max(1, reps // 4), 1)
+    keys = float(np.sum([np.sum(w.hist_len + L + t + 1) for t in range(w.steps)]))
+    b_dec = 2 * w.hkv * w.d * 2 * keys
+    out["decode"] = {"steps": w.steps, "ms_per_step": ms_turn / w.steps,
+                     "gbs": b_dec / ms_turn / 1e6,
+                     "frac_peak_hbm": b_dec / ms_turn / 1e6 / PEAK_HBM_GBS,
+                     "bytes": b_dec}
+    return out
+
+
+def cpu_baseline(w, budget_s=15.0):
+    """The fp64 oracle forward, as it stands, on a bounded sample of
+    workload 1: the first n (dialogue, head) pairs, n chosen from a one-pair
+    probe so that the run takes about budget_s; one pair per thread."""
+    import oracle
+    from paper_2408_00539_amd.workloads import bf16_bits_to_f32
+    from threadpoolctl import threadpool_limits
+    cores = len(os.sched_getaffinity(0))
+    q = bf16_bits_to_f32(w.q).astype(np.float64)
+    k = bf16_bits_to_f32(w.k).astype(np.float64)
+    v = bf16_bits_to_f32(w.v).astype(np.float64)
+    allpairs = [(b, h) for b in range(w.segs.batch) for h in range(w.hq)]
+
+    def run(pairs):
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            oracle.fwd(q, k, v, w.segs.cu_seqlens, w.segs.cu_segs,
+                       w.segs.seg_is_query, w.scale, pairs=pairs,
+                       workers=min(cores, len(pairs)))
+            return time.perf_counter() - t0
+
+    t1 = run(allpairs[:1])
+    n = int(min(len(allpairs), max(1, cores * int(budget_s / max(t1, 1e-3)))))
+    dt = run(allpairs[:n])
+    flop = 4 * w.d * sum(_pairs_of_dialogue(w.segs, b) for b, _ in allpairs[:n])
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"fp64 numpy oracle forward on {n} of {len(allpairs)} "
+                      f"(dialogue, head) pairs of workload 1, one pair per "
+                      f"thread, {dt:.1f} s wall",
+            "seconds": round(dt, 2), "cpu": _cpu_model()}
+
+
+def _pairs_of_dialogue(segs, b):
+    from types import SimpleNamespace
+    cu = segs.cu_seqlens
+    s, e = int(cu[b]), int(cu[b + 1])
+    cs = np.asarray(segs.cu_segs)
+    g0, g1 = int(np.searchsorted(cs, s)), int(np.searchsorted(cs, e))
+    return visible_pairs(SimpleNamespace(
+        cu_seqlens=np.array([0, e - s]), cu_segs=cs[g0:g1 + 1] - s,
+        seg_is_query=np.asarray(segs.seg_is_query)[g0:g1]))
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["step", "all"], default="all")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU "
+              "path (see the sharding design); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2408_00539_amd import ops, workloads as W
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    ops.lib()
+    timer = Timer()
+    with_bwd = _bwd_available()
+
+    log("generating workload 1 ...")
+    w1 = W.make_workload(1)
+    if with_bwd:
+        w1.do = W.packed_tensor(w1.seed, W.DO, w1.segs.cu_seqlens, w1.hq, w1.d)
+    torch.cuda.synchronize()
+    tr = bench_training(w1, timer, args.steps, args.warmup, with_bwd)
+    step_ms, step_flop = tr["step"]["ms"], tr["step"]["flop"]
+    log(f"step: {step_ms:.3f} ms, {step_flop / step_ms / 1e9:.1f} TFLOP/s")
+
+    paths = {"fwd": dict(tr["fwd"], workload="8x4096 h32 d128")}
+    dom_name, dom = "fwd_kernel", tr["fwd"]
+    if with_bwd:
+        paths["bwd_8x4096"] = dict(tr["bwd"], workload="8x4096 h32 d128")
+        dom_name, dom = "bwd kernels", tr["bwd"]
+    if args.only == "all":
+        log("generating workload 2 ...")
+        w2 = W.make_workload(2)
+        t2 = bench_training(w2, timer, 10, 2, False)
+        paths["fwd_gqa"] = dict(t2["fwd"], workload="2x16384 h32/kv8 d128")
+        del w2
+        if with_bwd:
+            log("generating workload 4 ...")
+            w4 = W.make_workload(4)
+            t4 = bench_training(w4, timer, 5, 1, True)
+            paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
+            del w4
+        log("generating workload 3 ...")
+        w3 = W.make_workload(3)
+        paths.update(bench_cache(w3, timer, 8, 2))
+        del w3
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        cpu = cpu_baseline(w1)
+
+    value = step_flop / step_ms / 1e9
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "ISM training step (prep+fwd" +
+                   ("+bwd" if with_bwd else "") + "), 8 dialogues x 4096 "
+                   "tokens, 8 turns, 32 heads, head_dim 128",
+                   "global_batch": 8, "seq_len": 4096, "heads": 32,
+                   "head_dim": 128, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "mfma", "kernel": dom_name,
+                     "achieved": round(dom["tflops"], 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(dom["tflops"] / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+        "paths": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
+                      for kk, vv in v.items()} for k, v in paths.items()},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def _bwd_available():
+    """True once the backward entry point runs on this build."""
+    import torch
+    from paper_2408_00539_amd import ops, workloads as W
+    segs_h = W.segments_from_lengths([[(4, True)]])
+    segs = ops.Segments.from_host(segs_h.cu_seqlens, segs_h.cu_segs,
+                                  segs_h.seg_is_query)
+    x = torch.zeros((4, 1, 64), dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros((1, 4), dtype=torch.float32, device="cuda")
+    try:
+        ops.bwd(x, x, x, x, lse, x, segs)
+        torch.cuda.synchronize()
+        return True
+    except ops.IsmError as e:
+        if e.status == 3:
+            return False
+        raise
+
+
+if __name__ == "__main__":
+    main()

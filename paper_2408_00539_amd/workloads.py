@@ -32,6 +32,8 @@ Workloads (all dialogue turns are [query, answer] pairs):
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -47,11 +49,22 @@ CACHE_CAP = 9216
 # bfloat16 helpers (bit patterns as uint16)
 # --------------------------------------------------------------------------
 
-def to_bf16_bits(x):
-    """float32 array -> bfloat16 bit patterns (round to nearest even)."""
+def to_bf16_bits(x, out=None):
+    """float32 array -> bfloat16 bit patterns (round to nearest even).
+
+    Written with in-place steps to keep large conversions to two passes of
+    fresh memory; ``out`` (uint16, same shape) receives the result if given.
+    """
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    r = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + r) >> np.uint32(16)).astype(np.uint16)
+    r = u >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    if out is None:
+        return r.astype(np.uint16)
+    np.copyto(out, r, casting="unsafe")
+    return out
 
 
 def bf16_bits_to_f32(b):
@@ -163,20 +176,34 @@ def alternating(lengths, first_is_query=True):
 # Tensors
 # --------------------------------------------------------------------------
 
-def normal_bf16(seed, code, b, shape):
+def normal_bf16(seed, code, b, shape, out=None):
     """N(0,1) bf16 bits of one dialogue's slice of one tensor."""
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(
         [int(seed), 1, int(code), int(b)])))
-    return to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    return to_bf16_bits(rng.standard_normal(shape, dtype=np.float32), out=out)
+
+
+def _pmap(fn, items):
+    """Run fn over items on a few threads (numpy's generators and
+    element-wise passes release the GIL)."""
+    items = list(items)
+    workers = max(1, min(16, len(os.sched_getaffinity(0)), len(items)))
+    if workers == 1:
+        return [fn(i) for i in items]
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        return list(ex.map(fn, items))
 
 
 def packed_tensor(seed, code, cu_seqlens, heads, d):
     """[T, heads, d] bf16 bits, generated dialogue by dialogue."""
     cu = np.asarray(cu_seqlens)
     out = np.empty((int(cu[-1]), heads, d), dtype=np.uint16)
-    for b in range(len(cu) - 1):
-        out[cu[b]:cu[b + 1]] = normal_bf16(seed, code, b,
-                                           (int(cu[b + 1] - cu[b]), heads, d))
+
+    def one(b):
+        normal_bf16(seed, code, b, (int(cu[b + 1] - cu[b]), heads, d),
+                    out=out[cu[b]:cu[b + 1]])
+
+    _pmap(one, range(len(cu) - 1))
     return out
 
 
@@ -289,9 +316,13 @@ def _make_cache_workload(seed, tensors, steps, batch):
         w.v_new = packed_tensor(seed, V_NEW, w.cu_new, H, d)
         w.k_cache = np.zeros((B, H, w.cache_cap, d), dtype=np.uint16)
         w.v_cache = np.zeros((B, H, w.cache_cap, d), dtype=np.uint16)
-        for b in range(B):
-            w.k_cache[b, :, :C] = history_slice(seed, K_HIST, b, H, C, d)
-            w.v_cache[b, :, :C] = history_slice(seed, V_HIST, b, H, C, d)
+
+        def hist_one(job):
+            b, code = job
+            dst = w.k_cache if code == K_HIST else w.v_cache
+            dst[b, :, :C] = history_slice(seed, code, b, H, C, d)
+
+        _pmap(hist_one, [(b, c) for b in range(B) for c in (K_HIST, V_HIST)])
         w.q_dec = np.stack([normal_bf16(seed, Q_DEC, b, (steps, H, d))
                             for b in range(B)], axis=1)
         w.k_dec = np.stack([normal_bf16(seed, K_DEC, b, (steps, H, d))

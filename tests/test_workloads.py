@@ -80,3 +80,14 @@ def test_cache_workload_small_batch_is_prefix():
     np.testing.assert_array_equal(
         w2.k_cache[0, :, :8192], W.history_slice(3, W.K_HIST, 0, 32, 8192, 128))
     assert not w2.k_cache[0, :, 8192:].any()
+
+
+def test_bench_flop_accounting_matches_oracle():
+    """bench.py counts useful pairs on its own; it must agree with the
+    oracle's count from the dense mask rule."""
+    import bench
+    import oracle
+    for i in (0, 1, 2, 4):
+        s = W.make_segments(i, i)
+        assert bench.visible_pairs(s) == oracle.visible_pairs(
+            s.cu_seqlens, s.cu_segs, s.seg_is_query)
