@@ -46,6 +46,15 @@ hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
   return hipGetLastError();
 }
 
+// Build-time tile configuration: rows per wave = 32 * ISM_FWD_NQB, and the
+// occupancy target in waves per SIMD (1 or 2) that bounds registers.
+#ifndef ISM_FWD_NQB
+#define ISM_FWD_NQB 1
+#endif
+#ifndef ISM_FWD_WPE
+#define ISM_FWD_WPE 2
+#endif
+
 namespace {
 
 constexpr int kBN = 64;  // keys per tile
@@ -54,67 +63,168 @@ template <int D>
 struct FwdSmem {
   static constexpr int KSTR = D + 8;  // padded K row (bank-conflict-free b128 reads)
   bf16_t k[2][kBN * KSTR];
-  bf16_t vt[2][D * kBN];              // V^T, 8-byte units XOR-swizzled by row
+  // V^T: one 128-byte row of 64 keys per head-dim index. Inside a row, key
+  // bits 2 and 3 are swapped so that the 8 keys one lane feeds to a P V
+  // MFMA are contiguous (one ds_read_b128), and the eight 16-byte chunks are
+  // XOR-swizzled with (row & 7) so that the 8 lanes of a read pass hit 8
+  // different chunks.
+  bf16_t vt[2][D * kBN];
 };
 
-// Stage one 64-key tile of K (row-major, padded) and V (transposed) through
-// registers. Keys past key_hi are clamped to key_hi (always valid memory);
-// they are masked out by the caller.
+// Byte offset of the 16-byte V^T chunk holding keys [32kb + 16bt + 8hf ..)
+// in storage order (see FwdSmem) for head-dim row d.
+__device__ __forceinline__ uint32_t vt_chunk(int d, int kb, int bt, int hf) {
+  return (uint32_t)(d * 128 + (((4 * kb + 2 * bt + hf) ^ (d & 7)) << 4));
+}
+
+// Stages one 64-key tile of K (row-major, padded) and V (transposed) through
+// registers. Thread-invariant address parts are computed once; a tile's base
+// is wave-uniform. Keys past the tile's valid count are clamped to the last
+// valid key (always valid memory); the caller masks them.
 template <int D>
 struct TileLoader {
   static constexpr int KCH = kBN * (D / 8) / 256;  // 16-byte K chunks per thread
+  static constexpr int RPI = 256 / (D / 8);         // K rows covered per chunk round
+  static constexpr int KSTR = FwdSmem<D>::KSTR;
   u32x4 kr[KCH];
   u32x4 vr[4];
+  uint32_t koff;   // byte offset of K chunk 0 of this thread inside a tile
+  uint32_t voff;   // byte offset of V row 4kg, chunk dc inside a tile
+  uint32_t kls;    // LDS byte offset of K chunk 0
+  uint32_t vls;    // LDS byte offset of V^T row dc*8, half (swap2(kg) & 1)
+  int krow, vrow, vch, rsb;
+  bool vjob;
 
-  __device__ __forceinline__ void load(const bf16_t *kbase, const bf16_t *vbase,
-                                       int64_t rs, int c0, int key_hi, int tid) {
+  __device__ __forceinline__ void init(int64_t rs, int tid) {
+    rsb = (int)(rs * 2);
+    krow = tid / (D / 8);
+    const int col = tid % (D / 8);
+    koff = (uint32_t)(krow * rsb + col * 16);
+    kls = (uint32_t)((krow * KSTR + col * 8) * 2);
+    vjob = tid < 16 * (D / 8);
+    const int kg = tid & 15, dc = tid >> 4;
+    vrow = 4 * kg;
+    voff = (uint32_t)(vrow * rsb + dc * 16);
+    const int u = ((kg & 1) << 1) | ((kg >> 1) & 1) | (kg & ~3);  // swap bits 0,1
+    vch = u >> 1;
+    vls = (uint32_t)(dc * 8 * 128 + (u & 1) * 8);
+  }
+
+  // tile = key base of the tile in global memory; nvalid = keys < 64 valid
+  __device__ __forceinline__ void load(const char *kt, const char *vt, int nvalid) {
+    if (nvalid >= kBN) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i;
-      const int row = c / (D / 8), col = c % (D / 8);
-      const int key = min(c0 + row, key_hi);
-      kr[i] = *(const u32x4 *)(kbase + (int64_t)key * rs + col * 8);
-    }
-    if (tid < 16 * (D / 8)) {
-      const int kg = tid & 15, dc = tid >> 4;
+      for (int i = 0; i < KCH; ++i)
+        kr[i] = *(const u32x4 *)(kt + (int64_t)(RPI * i) * rsb + koff);
+      if (vjob) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = min(c0 + 4 * kg + r, key_hi);
-        vr[r] = *(const u32x4 *)(vbase + (int64_t)key * rs + dc * 8);
+        for (int r = 0; r < 4; ++r)
+          vr[r] = *(const u32x4 *)(vt + (int64_t)r * rsb + voff);
+      }
+    } else {
+      const int last = nvalid - 1;
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int row = min(krow + RPI * i, last);
+        kr[i] = *(const u32x4 *)(kt + (int64_t)(row - krow) * rsb + koff);
+      }
+      if (vjob) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = min(vrow + r, last);
+          vr[r] = *(const u32x4 *)(vt + (int64_t)(row - vrow) * rsb + voff);
+        }
       }
     }
   }
 
-  __device__ __forceinline__ void store(FwdSmem<D> &sm, int buf, int tid) {
+  __device__ __forceinline__ void store(FwdSmem<D> &sm, int buf) {
+    char *kb = (char *)&sm.k[buf][0];
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i;
-      const int row = c / (D / 8), col = c % (D / 8);
-      *(u32x4 *)&sm.k[buf][row * FwdSmem<D>::KSTR + col * 8] = kr[i];
-    }
-    if (tid < 16 * (D / 8)) {
-      const int kg = tid & 15, dc = tid >> 4;
+    for (int i = 0; i < KCH; ++i)
+      *(u32x4 *)(kb + kls + i * RPI * KSTR * 2) = kr[i];
+    if (vjob) {
+      char *vb = (char *)&sm.vt[buf][0] + vls;
 #pragma unroll
       for (int dd = 0; dd < 8; ++dd) {
         const int m = dd >> 1;
-        uint32_t x0, x1;
-        if ((dd & 1) == 0) {
-          x0 = (vr[0][m] & 0xffffu) | (vr[1][m] << 16);
-          x1 = (vr[2][m] & 0xffffu) | (vr[3][m] << 16);
-        } else {
-          x0 = (vr[0][m] >> 16) | (vr[1][m] & 0xffff0000u);
-          x1 = (vr[2][m] >> 16) | (vr[3][m] & 0xffff0000u);
-        }
-        const int row = dc * 8 + dd;
-        const int pu = kg ^ (row & 15);
-        *(u32x2 *)&sm.vt[buf][row * kBN + pu * 4] = u32x2{x0, x1};
+        // keys 4kg..4kg+3 of head-dim index 8dc+dd, packed as two bf16 pairs
+        const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t x0 = __builtin_amdgcn_perm(vr[1][m], vr[0][m], sel);
+        const uint32_t x1 = __builtin_amdgcn_perm(vr[3][m], vr[2][m], sel);
+        *(u32x2 *)(vb + dd * 128 + ((vch ^ dd) << 4)) = u32x2{x0, x1};
       }
     }
   }
 };
 
+// Online softmax of one 64-key tile held as S^T accumulators (lane <->
+// query row; the other 32 keys of the row sit in lane l ^ 32). Writes the
+// bf16 probabilities as B operands of the P V product.
+template <bool MASK, int NQB, int NDB>
+__device__ __forceinline__ void softmax_tile(f32x16 (&sacc)[2][NQB], int c0, int hf,
+                                             const int (&lim_r)[NQB], float sl2, float tau,
+                                             float (&m_run)[NQB], float (&l_run)[NQB],
+                                             f32x16 (&oacc)[NDB][NQB],
+                                             bf16x8 (&pf)[NQB][2][2]) {
+  float mt[NQB];
+  bool grow = false;
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    float x = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (MASK) {
+          const int key = c0 + kb * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+          if (key > lim_r[qb]) sacc[kb][qb][r] = -INFINITY;
+        }
+        x = fmaxf(x, sacc[kb][qb][r]);
+      }
+    mt[qb] = pair_max(x);
+    grow |= mt[qb] > m_run[qb] + tau;
+  }
+  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) {
+      const float mnew = fmaxf(m_run[qb], mt[qb]);
+      const float alpha = fast_exp2((m_run[qb] - mnew) * sl2);
+      m_run[qb] = mnew;
+      l_run[qb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][qb][r] *= alpha;
+    }
+  }
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    const float moff = m_run[qb] * sl2;
+    float rsum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int bt = 0; bt < 2; ++bt) {
+        f32x2 p[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          p[u][0] = fast_exp2(fmaf(sacc[kb][qb][8 * bt + 2 * u], sl2, -moff));
+          p[u][1] = fast_exp2(fmaf(sacc[kb][qb][8 * bt + 2 * u + 1], sl2, -moff));
+          rsum += p[u][0] + p[u][1];
+        }
+        u32x4 w;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) w[u] = cvt_bf16x2(p[u]);
+        pf[qb][kb][bt] = __builtin_bit_cast(bf16x8, w);
+      }
+    l_run[qb] += rsum;
+  }
+}
+
 template <int D, int NQB, bool CACHE>
 __global__ void __launch_bounds__(256)
+__attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
 fwd_kernel(FwdArgs a, int hpw, int tiles) {
   constexpr int QW = NQB * 32;     // rows per wave
   constexpr int KSTR = FwdSmem<D>::KSTR;
@@ -194,99 +304,62 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
 
+  // lazy rescaling: the running max is only raised when a row's tile max
+  // exceeds it by more than 2^8 in probability units (exact either way:
+  // numerator and denominator share the reference max)
+  const float tau = 8.f / sl2;
+  bf16x8 pf[NQB][2][2];
+
   const int ntiles = (key_hi - key_begin) / kBN + 1;
   TileLoader<D> ld;
-  ld.load(kbase, vbase, rs, key_begin, key_hi, tid);
-  ld.store(sm, 0, tid);
+  ld.init(rs, tid);
+  const int64_t tile_bytes = (int64_t)kBN * rs * 2;
+  const char *kt = (const char *)(kbase + (int64_t)key_begin * rs);
+  const char *vt = (const char *)(vbase + (int64_t)key_begin * rs);
+  ld.load(kt, vt, key_hi - key_begin + 1);
+  ld.store(sm, 0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
     const int c0 = key_begin + t * kBN;
-    if (t + 1 < ntiles) ld.load(kbase, vbase, rs, c0 + kBN, key_hi, tid);
+    if (t + 1 < ntiles) {
+      kt += tile_bytes;
+      vt += tile_bytes;
+      ld.load(kt, vt, key_hi - (c0 + kBN) + 1);
+    }
 
     if (active && c0 <= wave_hi) {
-      const bool full = c0 + kBN - 1 <= wave_lo;
       // S^T[key][row] for two 32-key blocks
       f32x16 sacc[2][NQB];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int qb = 0; qb < NQB; ++qb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sacc[kb][qb][r] = 0.f;
         const bf16_t *kp = &sm.k[buf][(kb * 32 + l32) * KSTR + hf * 8];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
           const bf16x8 kf = *(const bf16x8 *)(kp + ks * 16);
 #pragma unroll
           for (int qb = 0; qb < NQB; ++qb)
-            sacc[kb][qb] = mfma32x32x16(kf, qf[qb][ks], sacc[kb][qb]);
+            sacc[kb][qb] = mfma32x32x16(kf, qf[qb][ks], ks == 0 ? f32x16{} : sacc[kb][qb]);
         }
       }
-
-      // online softmax, one query row per lane (pair)
-      bf16x8 pf[NQB][2][2];
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) {
-        float mt = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            float x = sacc[kb][qb][r];
-            if (!full) {
-              const int key = c0 + kb * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-              if (key > lim_r[qb]) x = -INFINITY;
-              sacc[kb][qb][r] = x;
-            }
-            mt = fmaxf(mt, x);
-          }
-        mt = fmaxf(mt, swap_halves(mt));
-        const float mnew = fmaxf(m_run[qb], mt);
-        const float alpha = fast_exp2((m_run[qb] - mnew) * sl2);
-        m_run[qb] = mnew;
-        const float moff = mnew * sl2;
-        float rsum = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int bt = 0; bt < 2; ++bt) {
-            float p[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-              p[u] = fast_exp2(fmaf(sacc[kb][qb][8 * bt + u], sl2, -moff));
-              rsum += p[u];
-            }
-            u32x4 w;
-            w[0] = pack_bf16x2(p[0], p[1]);
-            w[1] = pack_bf16x2(p[2], p[3]);
-            w[2] = pack_bf16x2(p[4], p[5]);
-            w[3] = pack_bf16x2(p[6], p[7]);
-            pf[qb][kb][bt] = __builtin_bit_cast(bf16x8, w);
-          }
-        l_run[qb] = fmaf(l_run[qb], alpha, rsum);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[db][qb][r] *= alpha;
+      // only tiles that cross some row's bound pay for the mask
+      if (c0 + kBN - 1 <= wave_lo) {
+        softmax_tile<false>(sacc, c0, hf, lim_r, sl2, tau, m_run, l_run, oacc, pf);
+      } else {
+        softmax_tile<true>(sacc, c0, hf, lim_r, sl2, tau, m_run, l_run, oacc, pf);
       }
 
       // O^T[d][row] += V^T[d][key] P^T[key][row]
+      const char *vtb = (const char *)&sm.vt[buf][0];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const int d = db * 32 + l32;
-        const bf16_t *vrow = &sm.vt[buf][d * kBN];
-        const int sw = l32 & 15;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int bt = 0; bt < 2; ++bt) {
-            const int u1 = kb * 8 + 4 * bt + hf;
-            const u32x2 lo = *(const u32x2 *)(vrow + ((u1 ^ sw) * 4));
-            const u32x2 hi = *(const u32x2 *)(vrow + (((u1 + 2) ^ sw) * 4));
-            const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-            const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+            const bf16x8 vf =
+                *(const bf16x8 *)(vtb + vt_chunk(db * 32 + l32, kb, bt, hf));
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb)
               oacc[db][qb] = mfma32x32x16(vf, pf[qb][kb][bt], oacc[db][qb]);
@@ -294,14 +367,14 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
       }
     }
 
-    if (t + 1 < ntiles) ld.store(sm, buf ^ 1, tid);
+    if (t + 1 < ntiles) ld.store(sm, buf ^ 1);
     __syncthreads();
   }
 
   if (!active) return;
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
-    const float lt = l_run[qb] + swap_halves(l_run[qb]);
+    const float lt = pair_sum(l_run[qb]);
     const int row = wq0 + qb * 32 + l32;
     if (row >= e) continue;
     const float inv = 1.f / lt;
@@ -327,7 +400,7 @@ int gcd_int(int x, int y) {
 
 template <int D, bool CACHE>
 hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
-  constexpr int NQB = 2;
+  constexpr int NQB = ISM_FWD_NQB;
   const int hpw = gcd_int(a.hq / a.hkv, 4);
   const int wg_rows = (4 / hpw) * NQB * 32;
   const int tiles = (a.max_rows + wg_rows - 1) / wg_rows;
