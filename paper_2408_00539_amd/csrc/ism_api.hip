@@ -105,7 +105,7 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
     case ISM_OP_FWD:
       return align_up((size_t)total_tokens * 4);
     case ISM_OP_BWD:
-      return align_up((size_t)total_tokens * 4) +
+      return 2 * align_up((size_t)total_tokens * 4) +
              align_up((size_t)total_tokens * hq * 4);
     case ISM_OP_PREFILL_CACHED:
       return 0;
@@ -173,17 +173,19 @@ extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
   if ((st = check_device())) return st;
 
   hipStream_t s = (hipStream_t)stream;
+  const size_t tb = align_up((size_t)sg->total_tokens * 4);
   int32_t *lim = (int32_t *)ws;
-  float *delta = (float *)((char *)ws + align_up((size_t)sg->total_tokens * 4));
-  if ((st = hip_status(ism::launch_prep_lim(sg->cu_segs, sg->seg_is_query, sg->num_segs,
-                                            sg->total_tokens, lim, s),
+  int32_t *seer = (int32_t *)((char *)ws + tb);
+  float *delta = (float *)((char *)ws + 2 * tb);
+  if ((st = hip_status(ism::launch_bwd_prep(sg->cu_segs, sg->seg_is_query, sg->num_segs,
+                                            sg->total_tokens, lim, seer, s),
                        "prep launch")))
     return st;
   ism::BwdArgs a{};
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse;
   a.dq = dq; a.dk = dk; a.dv = dv; a.delta = delta;
   a.cu_seqlens = sg->cu_seqlens; a.cu_segs = sg->cu_segs;
-  a.seg_is_query = sg->seg_is_query; a.lim = lim;
+  a.seg_is_query = sg->seg_is_query; a.lim = lim; a.seer = seer;
   a.batch = sg->batch; a.num_segs = sg->num_segs; a.hq = hq; a.hkv = hkv;
   a.total = sg->total_tokens; a.max_seqlen = sg->max_seqlen;
   a.scale = scale; a.deterministic = deterministic;

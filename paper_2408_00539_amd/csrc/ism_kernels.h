@@ -73,11 +73,16 @@ struct BwdArgs {
   const int32_t *cu_seqlens;
   const int32_t *cu_segs;
   const uint8_t *seg_is_query;
-  const int32_t *lim;       // [T]
+  const int32_t *lim;       // [T] inclusive key bound per row
+  const int32_t *seer;      // [T] first row that sees each key
   int32_t batch, num_segs, hq, hkv, total, max_seqlen;
   float scale;
   int32_t deterministic;
 };
+
+hipError_t launch_bwd_prep(const int32_t *cu_segs, const uint8_t *seg_is_query,
+                           int32_t num_segs, int32_t total, int32_t *lim, int32_t *seer,
+                           hipStream_t stream);
 
 hipError_t launch_bwd(const BwdArgs &a, int d, hipStream_t stream);
 
