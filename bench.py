@@ -254,7 +254,7 @@ def main():
     dom_name, dom = "fwd_kernel", tr["fwd"]
     if with_bwd:
         paths["bwd_8x4096"] = dict(tr["bwd"], workload="8x4096 h32 d128")
-        dom_name, dom = "bwd kernels", tr["bwd"]
+        dom_name, dom = "ism_attn_bwd (delta_kernel + dkv_kernel + dq_kernel)", tr["bwd"]
     if args.only == "all":
         log("generating workload 2 ...")
         w2 = W.make_workload(2)
