@@ -27,6 +27,10 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+# per-source extras: the backward keeps MFMA accumulators in VGPRs (the
+# default AGPR form made the dK/dV kernel shuttle values between register
+# files on every tile)
+EXTRA_FLAGS = {"ism_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc():
@@ -39,7 +43,8 @@ def hipcc():
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     if src.endswith(".hip"):
-        cmd = [hipcc(), *HIP_FLAGS, "-c", src, "-o", obj]
+        cmd = [hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []),
+               "-c", src, "-o", obj]
     else:
         cmd = [os.environ.get("CXX", "g++"), *HOST_FLAGS, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -82,52 +82,36 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 
 template <int D>
 struct DkvSmem {
-  static constexpr int STR = D + 8;  // padded row-major rows
-  bf16_t q[2][kBR * STR];
-  bf16_t dout[2][kBR * STR];
-  // transposed tiles: head-dim row d holds the 32 rows (64 bytes, four
-  // 16-byte chunks); row bits 2 and 3 swapped so that one lane's 8 operand
-  // rows are contiguous; chunks XOR-swizzled with ((d >> 1) & 3).
-  bf16_t qt[2][D * kBR];
-  bf16_t dt[2][D * kBR];
+  static constexpr int STR = D + 8;  // padded rows: conflict-free ds_read_b128
+  bf16_t q[2][kBR * STR];           // row-major; transposed operands come
+  bf16_t dout[2][kBR * STR];        // from ds_read_b64_tr_b16 (tr_operand)
   float lse2[2][kBR];
   float delta[2][kBR];
   int lim[2][kBR];
 };
 
-__device__ __forceinline__ uint32_t t32_chunk(int d, int bt, int hf) {
-  return (uint32_t)(d * 64 + (((2 * bt + hf) ^ ((d >> 1) & 3)) << 4));
-}
-
-// One 32-row tile of Q (threads 0..) and dO (threads 128..), 4 rows x 16 bytes
-// per job, written row-major and transposed; threads 224..255 also stage the
-// per-row LSE (as log2), delta and lim (lim = -1 marks rows past the end).
+// One 32-row tile of Q and dO, row-major, 16-byte chunks; threads 224..255
+// also stage the per-row LSE (as log2), delta and lim (lim = -1 marks rows
+// past the end of the dialogue).
 template <int D>
 struct RowTileLoader {
-  static constexpr int JOBS = 8 * (D / 8);
-  u32x4 r[4];
+  static constexpr int CPR = D / 8;              // chunks per row
+  static constexpr int CH = kBR * CPR / 256;     // chunks per thread per tensor
+  u32x4 rq[CH], rd[CH];
   float l2, dl;
   int lm;
-  int job, rg, dc;
-  bool isq, has_job, has_row;
+  bool has_row;
 
-  __device__ __forceinline__ void init(int tid) {
-    isq = tid < 128;
-    job = isq ? tid : tid - 128;
-    has_job = job < JOBS;
-    rg = job & 7;
-    dc = job >> 3;
-    has_row = tid >= 224;
-  }
+  __device__ __forceinline__ void init(int tid) { has_row = tid >= 224; }
 
-  __device__ __forceinline__ void load(const BwdArgs &a, int r0, int e, int h, int D_) {
-    if (has_job) {
-      const bf16_t *src = (const bf16_t *)(isq ? a.q : a.dout);
+  __device__ __forceinline__ void load(const BwdArgs &a, int r0, int e, int h) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = min(r0 + 4 * rg + i, e - 1);
-        r[i] = *(const u32x4 *)(src + ((int64_t)row * a.hq + h) * D_ + dc * 8);
-      }
+    for (int i = 0; i < CH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int row = min(r0 + c / CPR, e - 1), col = c % CPR;
+      const int64_t off = ((int64_t)row * a.hq + h) * D + col * 8;
+      rq[i] = *(const u32x4 *)((const bf16_t *)a.q + off);
+      rd[i] = *(const u32x4 *)((const bf16_t *)a.dout + off);
     }
     if (has_row) {
       const int row = r0 + (threadIdx.x - 224);
@@ -141,22 +125,12 @@ struct RowTileLoader {
 
   __device__ __forceinline__ void store(DkvSmem<D> &sm, int buf) {
     constexpr int STR = DkvSmem<D>::STR;
-    if (has_job) {
-      bf16_t *rm = isq ? sm.q[buf] : sm.dout[buf];
-      char *tr = (char *)(isq ? sm.qt[buf] : sm.dt[buf]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) *(u32x4 *)&rm[(4 * rg + i) * STR + dc * 8] = r[i];
-      const int u = ((rg & 1) << 1) | ((rg >> 1) & 1) | (rg & ~3);
-      const int ch = u >> 1, half = u & 1;
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int m = dd >> 1;
-        const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t x0 = __builtin_amdgcn_perm(r[1][m], r[0][m], sel);
-        const uint32_t x1 = __builtin_amdgcn_perm(r[3][m], r[2][m], sel);
-        const int d = dc * 8 + dd;
-        *(u32x2 *)(tr + d * 64 + ((ch ^ ((d >> 1) & 3)) << 4) + half * 8) = u32x2{x0, x1};
-      }
+    for (int i = 0; i < CH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int row = c / CPR, col = c % CPR;
+      *(u32x4 *)&sm.q[buf][row * STR + col * 8] = rq[i];
+      *(u32x4 *)&sm.dout[buf][row * STR + col * 8] = rd[i];
     }
     if (has_row) {
       const int rr = threadIdx.x - 224;
@@ -213,7 +187,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int iters = G * nrt;
   RowTileLoader<D> ld;
   ld.init(tid);
-  ld.load(a, rstart, e, kvh * G, D);
+  ld.load(a, rstart, e, kvh * G);
   ld.store(sm, 0);
   __syncthreads();
 
@@ -222,7 +196,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
     const int r0 = rstart + (it % nrt) * kBR;
     if (it + 1 < iters) {
       const int g1 = (it + 1) / nrt, rt1 = (it + 1) % nrt;
-      ld.load(a, rstart + rt1 * kBR, e, kvh * G + g1, D);
+      ld.load(a, rstart + rt1 * kBR, e, kvh * G + g1);
     }
     const int nvalid = min(kBR, e - r0);
     const int lim_last = sm.lim[buf][nvalid - 1];
@@ -268,15 +242,15 @@ dkv_kernel(BwdArgs a, int ktiles) {
         pfr[bt] = __builtin_bit_cast(bf16x8, wp);
         dsf[bt] = __builtin_bit_cast(bf16x8, wd);
       }
-      const char *dot = (const char *)sm.dt[buf];
-      const char *qtt = (const char *)sm.qt[buf];
+      // dV^T[d][key] += dO^T P, dK^T[d][key] += Q^T dS (contraction over rows)
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int bt = 0; bt < 2; ++bt) {
-          const uint32_t off = t32_chunk(db * 32 + l32, bt, hf);
-          dv[db] = mfma32x32x16(*(const bf16x8 *)(dot + off), pfr[bt], dv[db]);
-          dk[db] = mfma32x32x16(*(const bf16x8 *)(qtt + off), dsf[bt], dk[db]);
+          dv[db] = mfma32x32x16(tr_operand(sm.dout[buf], STR, db * 32, 16 * bt, lane),
+                                pfr[bt], dv[db]);
+          dk[db] = mfma32x32x16(tr_operand(sm.q[buf], STR, db * 32, 16 * bt, lane),
+                                dsf[bt], dk[db]);
         }
     }
     if (it + 1 < iters) ld.store(sm, buf ^ 1);
@@ -307,60 +281,37 @@ dkv_kernel(BwdArgs a, int ktiles) {
 template <int D>
 struct DqSmem {
   static constexpr int STR = D + 8;
-  bf16_t k[kBK * STR];   // row-major K tile (A operand of S^T = K Q^T)
-  bf16_t v[kBK * STR];   // row-major V tile (A operand of dP^T = V dO^T)
-  bf16_t kt[D * kBK];    // K^T, same storage order as the forward's V^T
+  bf16_t k[kBK * STR];   // row-major K tile: A operand of S^T = K Q^T, and
+                         // (through tr_operand) of dQ^T = K^T dS^T
+  bf16_t v[kBK * STR];   // row-major V tile: A operand of dP^T = V dO^T
 };
 
-__device__ __forceinline__ uint32_t t64_chunk(int d, int kb, int bt, int hf) {
-  return (uint32_t)(d * 128 + (((4 * kb + 2 * bt + hf) ^ (d & 7)) << 4));
-}
-
-// One 64-key tile of K and V: thread job (kg, dc) covers keys 4kg..4kg+3,
-// head-dim chunk dc, for both tensors; K is also written transposed.
+// One 64-key tile of K and V, row-major 16-byte chunks.
 template <int D>
 struct KeyTileLoader {
-  static constexpr int JOBS = 16 * (D / 8);
-  u32x4 kr[4], vr[4];
-  int kg, dc;
-  bool has_job;
-
-  __device__ __forceinline__ void init(int tid) {
-    has_job = tid < JOBS;
-    kg = tid & 15;
-    dc = tid >> 4;
-  }
+  static constexpr int CPR = D / 8;
+  static constexpr int CH = kBK * CPR / 256;
+  u32x4 kr[CH], vr[CH];
 
   __device__ __forceinline__ void load(const bf16_t *kb, const bf16_t *vb, int64_t rs,
                                        int c0, int key_hi) {
-    if (!has_job) return;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int key = min(c0 + 4 * kg + r, key_hi);
-      kr[r] = *(const u32x4 *)(kb + (int64_t)key * rs + dc * 8);
-      vr[r] = *(const u32x4 *)(vb + (int64_t)key * rs + dc * 8);
+    for (int i = 0; i < CH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int key = min(c0 + c / CPR, key_hi), col = c % CPR;
+      kr[i] = *(const u32x4 *)(kb + (int64_t)key * rs + col * 8);
+      vr[i] = *(const u32x4 *)(vb + (int64_t)key * rs + col * 8);
     }
   }
 
   __device__ __forceinline__ void store(DqSmem<D> &sm) {
     constexpr int STR = DqSmem<D>::STR;
-    if (!has_job) return;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      *(u32x4 *)&sm.k[(4 * kg + r) * STR + dc * 8] = kr[r];
-      *(u32x4 *)&sm.v[(4 * kg + r) * STR + dc * 8] = vr[r];
-    }
-    const int u = ((kg & 1) << 1) | ((kg >> 1) & 1) | (kg & ~3);
-    const int ch = u >> 1, half = u & 1;
-    char *tr = (char *)sm.kt;
-#pragma unroll
-    for (int dd = 0; dd < 8; ++dd) {
-      const int m = dd >> 1;
-      const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
-      const uint32_t x0 = __builtin_amdgcn_perm(kr[1][m], kr[0][m], sel);
-      const uint32_t x1 = __builtin_amdgcn_perm(kr[3][m], kr[2][m], sel);
-      const int d = dc * 8 + dd;
-      *(u32x2 *)(tr + d * 128 + ((ch ^ (d & 7)) << 4) + half * 8) = u32x2{x0, x1};
+    for (int i = 0; i < CH; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      const int row = c / CPR, col = c % CPR;
+      *(u32x4 *)&sm.k[row * STR + col * 8] = kr[i];
+      *(u32x4 *)&sm.v[row * STR + col * 8] = vr[i];
     }
   }
 };
@@ -419,7 +370,6 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const int64_t rs = (int64_t)a.hkv * D;
   const int ntiles = (key_hi - s) / kBK + 1;
   KeyTileLoader<D> ld;
-  ld.init(tid);
   ld.load(kbase, vbase, rs, s, key_hi);
 
   for (int t = 0; t < ntiles; ++t) {
@@ -459,12 +409,11 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
           for (int u = 0; u < 4; ++u) x[u] = cvt_bf16x2(w[u]);
           dsf[bt] = __builtin_bit_cast(bf16x8, x);
         }
-        const char *ktt = (const char *)sm.kt;
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
 #pragma unroll
           for (int bt = 0; bt < 2; ++bt)
-            dq[db] = mfma32x32x16(*(const bf16x8 *)(ktt + t64_chunk(db * 32 + l32, kb, bt, hf)),
+            dq[db] = mfma32x32x16(tr_operand(sm.k, STR, db * 32, kb * 32 + 16 * bt, lane),
                                   dsf[bt], dq[db]);
       }
     }

@@ -63,6 +63,28 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return cvt_bf16x2(f32x2{lo, hi});
 }
 
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// A operand (32 x 16, bf16) of a 32x32x16 MFMA read from a tile stored with
+// the MFMA k index as the row: tile[k * str + m]. Lane l receives row
+// m0 + (l % 32) and k = k0 + 4h + {0..3} (slots 0-3), k0 + 8 + 4h + {0..3}
+// (slots 4-7), h = l / 32, through two ds_read_b64_tr_b16. That transposing
+// read works per 16-lane group: output lane r gets element r % 4 of the
+// 8-byte loads of lanes r/4, r/4 + 4, r/4 + 8, r/4 + 12; so lane L of a group
+// loads tile row k0 + 4h + L/4, columns m + 4 (L % 4) .. + 3.
+__device__ __forceinline__ bf16x8 tr_operand(const bf16_t *tile, int str, int m0, int k0,
+                                             int lane) {
+  const int g = lane >> 4, L = lane & 15;
+  const int m = m0 + 16 * (g & 1) + 4 * (L & 3);
+  const int k = k0 + 4 * (g >> 1) + (L >> 2);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + k * str + m));
+  const i16x4 hi =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + (k + 8) * str + m));
+  const i16x4 v[2] = {lo, hi};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) {
   return __builtin_bit_cast(float, w << 16);
 }
