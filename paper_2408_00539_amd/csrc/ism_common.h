@@ -85,6 +85,99 @@ __device__ __forceinline__ bf16x8 tr_operand(const bf16_t *tile, int str, int m0
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// Row swizzle of 16-byte chunks in unpadded LDS tiles: logical chunk c of
+// tile row r is stored at chunk c ^ swz(r). With 128- or 256-byte rows this
+// is conflict-free both for ds_read_b128 of 8 consecutive rows at one chunk
+// and for the 4 consecutive rows x 32 bytes of a ds_read_b64_tr_b16 group.
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+// Wait until this wave's outstanding vector-memory operations, including
+// global->LDS transfers, have completed.
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Direct global->LDS staging of a ROWS x D bf16 tile (unpadded, swizzled)
+// by the 4 waves of a workgroup. Each global_load_lds_dwordx4 writes lane l's
+// 16 bytes to LDS bytes [16 l, 16 l + 16) of a 1 KB block, so the swizzle is
+// applied by choosing each lane's source chunk. No registers hold the data.
+template <int D, int ROWS>
+struct DmaTile {
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;       // rows per 1 KB transfer
+  static constexpr int NI = ROWS / RPI / 4;  // transfers per wave
+  static_assert(NI >= 1 && ROWS % (4 * RPI) == 0, "tile not divisible among 4 waves");
+  uint32_t loff[NI];  // element offset of this lane's source chunk (full tile)
+  int wave, lane;
+
+  __device__ __forceinline__ void init(int tid, int64_t rs) {
+    wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    lane = tid & 63;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = (wave * NI + i) * RPI + lane / CPR;
+      loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz(r)) * 8);
+    }
+  }
+
+  // Rows [0, ROWS) of the tile starting at src (row stride rs elements); rows
+  // at or past nvalid repeat row nvalid - 1 (always valid memory).
+  __device__ __forceinline__ void issue(const bf16_t *src, int64_t rs, int nvalid,
+                                        bf16_t *lds) const {
+    typedef __attribute__((address_space(3))) void lds_void;
+    if (__builtin_amdgcn_readfirstlane(nvalid) >= ROWS) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        __builtin_amdgcn_global_load_lds((const void *)(src + loff[i]),
+                                         (lds_void *)(lds + (wave * NI + i) * 512), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int r = (wave * NI + i) * RPI + lane / CPR;
+        const int rr = min(r, nvalid - 1);
+        const bf16_t *g = src + (int64_t)rr * rs + ((lane % CPR) ^ swz(r)) * 8;
+        __builtin_amdgcn_global_load_lds((const void *)g,
+                                         (lds_void *)(lds + (wave * NI + i) * 512), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// A operand from a swizzled unpadded tile through two transposing reads, at
+// precomputed byte offsets (see tr_operand for the lane mapping).
+__device__ __forceinline__ bf16x8 tr_operand_at(const char *lds, uint32_t off_lo,
+                                                uint32_t off_hi) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(lds + off_lo));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(lds + off_hi));
+  const i16x4 v[2] = {lo, hi};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Per-lane byte offsets for reading MFMA A operands from a swizzled,
+// unpadded tile with RB-byte rows.
+//  * row operand (ds_read_b128): row r0 + (lane % 32) with r0 % 8 == 0, head
+//    chunks 2ks + h: offset = row(r0) + 128 (ks / 4) + rowk[ks % 4];
+//  * transposed operand (tr reads): rows k0 + 4h + lane_row, k0 % 16 == 0,
+//    columns 32 db + ...: offset = (db odd ? tro : tre) + 64 db + row(k0),
+//    and + 8 rows for the second read.
+struct SwzOffsets {
+  uint32_t rowk[4];
+  uint32_t tre, tro;
+
+  __device__ __forceinline__ void init(int lane, int rb) {
+    const int l32 = lane & 31, h = lane >> 5;
+    const int f = swz(l32);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) rowk[b] = (uint32_t)(l32 * rb + (((2 * b + h) ^ f) << 4));
+    const int g = lane >> 4, L = lane & 15, gh = g >> 1;
+    const int fv = ((L >> 2) << 1) | gh;
+    const int y = (2 * (g & 1) + ((L & 3) >> 1)) ^ fv;
+    const int yo = y - 8 * ((y >> 2) & 1);
+    const int base = (4 * gh + (L >> 2)) * rb + 8 * (L & 1);
+    tre = (uint32_t)(base + 16 * y);
+    tro = (uint32_t)(base + 16 * yo);
+  }
+};
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) {
   return __builtin_bit_cast(float, w << 16);
 }

@@ -59,103 +59,14 @@ namespace {
 
 constexpr int kBN = 64;  // keys per tile
 
+// K and V tiles of 64 keys, row-major, unpadded rows of D bf16 with the
+// swz() chunk swizzle, double-buffered; filled by direct global->LDS
+// transfers. K is read as MFMA rows (ds_read_b128), V through transposing
+// reads (ds_read_b64_tr_b16) as the V^T operand.
 template <int D>
 struct FwdSmem {
-  static constexpr int KSTR = D + 8;  // padded K row (bank-conflict-free b128 reads)
-  bf16_t k[2][kBN * KSTR];
-  // V^T: one 128-byte row of 64 keys per head-dim index. Inside a row, key
-  // bits 2 and 3 are swapped so that the 8 keys one lane feeds to a P V
-  // MFMA are contiguous (one ds_read_b128), and the eight 16-byte chunks are
-  // XOR-swizzled with (row & 7) so that the 8 lanes of a read pass hit 8
-  // different chunks.
-  bf16_t vt[2][D * kBN];
-};
-
-// Byte offset of the 16-byte V^T chunk holding keys [32kb + 16bt + 8hf ..)
-// in storage order (see FwdSmem) for head-dim row d.
-__device__ __forceinline__ uint32_t vt_chunk(int d, int kb, int bt, int hf) {
-  return (uint32_t)(d * 128 + (((4 * kb + 2 * bt + hf) ^ (d & 7)) << 4));
-}
-
-// Stages one 64-key tile of K (row-major, padded) and V (transposed) through
-// registers. Thread-invariant address parts are computed once; a tile's base
-// is wave-uniform. Keys past the tile's valid count are clamped to the last
-// valid key (always valid memory); the caller masks them.
-template <int D>
-struct TileLoader {
-  static constexpr int KCH = kBN * (D / 8) / 256;  // 16-byte K chunks per thread
-  static constexpr int RPI = 256 / (D / 8);         // K rows covered per chunk round
-  static constexpr int KSTR = FwdSmem<D>::KSTR;
-  u32x4 kr[KCH];
-  u32x4 vr[4];
-  uint32_t koff;   // byte offset of K chunk 0 of this thread inside a tile
-  uint32_t voff;   // byte offset of V row 4kg, chunk dc inside a tile
-  uint32_t kls;    // LDS byte offset of K chunk 0
-  uint32_t vls;    // LDS byte offset of V^T row dc*8, half (swap2(kg) & 1)
-  int krow, vrow, vch, rsb;
-  bool vjob;
-
-  __device__ __forceinline__ void init(int64_t rs, int tid) {
-    rsb = (int)(rs * 2);
-    krow = tid / (D / 8);
-    const int col = tid % (D / 8);
-    koff = (uint32_t)(krow * rsb + col * 16);
-    kls = (uint32_t)((krow * KSTR + col * 8) * 2);
-    vjob = tid < 16 * (D / 8);
-    const int kg = tid & 15, dc = tid >> 4;
-    vrow = 4 * kg;
-    voff = (uint32_t)(vrow * rsb + dc * 16);
-    const int u = ((kg & 1) << 1) | ((kg >> 1) & 1) | (kg & ~3);  // swap bits 0,1
-    vch = u >> 1;
-    vls = (uint32_t)(dc * 8 * 128 + (u & 1) * 8);
-  }
-
-  // tile = key base of the tile in global memory; nvalid = keys < 64 valid
-  __device__ __forceinline__ void load(const char *kt, const char *vt, int nvalid) {
-    if (nvalid >= kBN) {
-#pragma unroll
-      for (int i = 0; i < KCH; ++i)
-        kr[i] = *(const u32x4 *)(kt + (int64_t)(RPI * i) * rsb + koff);
-      if (vjob) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          vr[r] = *(const u32x4 *)(vt + (int64_t)r * rsb + voff);
-      }
-    } else {
-      const int last = nvalid - 1;
-#pragma unroll
-      for (int i = 0; i < KCH; ++i) {
-        const int row = min(krow + RPI * i, last);
-        kr[i] = *(const u32x4 *)(kt + (int64_t)(row - krow) * rsb + koff);
-      }
-      if (vjob) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = min(vrow + r, last);
-          vr[r] = *(const u32x4 *)(vt + (int64_t)(row - vrow) * rsb + voff);
-        }
-      }
-    }
-  }
-
-  __device__ __forceinline__ void store(FwdSmem<D> &sm, int buf) {
-    char *kb = (char *)&sm.k[buf][0];
-#pragma unroll
-    for (int i = 0; i < KCH; ++i)
-      *(u32x4 *)(kb + kls + i * RPI * KSTR * 2) = kr[i];
-    if (vjob) {
-      char *vb = (char *)&sm.vt[buf][0] + vls;
-#pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        const int m = dd >> 1;
-        // keys 4kg..4kg+3 of head-dim index 8dc+dd, packed as two bf16 pairs
-        const uint32_t sel = (dd & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t x0 = __builtin_amdgcn_perm(vr[1][m], vr[0][m], sel);
-        const uint32_t x1 = __builtin_amdgcn_perm(vr[3][m], vr[2][m], sel);
-        *(u32x2 *)(vb + dd * 128 + ((vch ^ dd) << 4)) = u32x2{x0, x1};
-      }
-    }
-  }
+  bf16_t k[2][kBN * D];
+  bf16_t v[2][kBN * D];
 };
 
 // Online softmax of one 64-key tile held as S^T accumulators (lane <->
@@ -227,7 +138,6 @@ __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
 fwd_kernel(FwdArgs a, int hpw, int tiles) {
   constexpr int QW = NQB * 32;     // rows per wave
-  constexpr int KSTR = FwdSmem<D>::KSTR;
   constexpr int NDB = D / 32;      // 32-wide d blocks of the output
   constexpr int NKS = D / 16;      // 16-deep k steps of Q K^T
   __shared__ FwdSmem<D> sm;
@@ -311,33 +221,38 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
   bf16x8 pf[NQB][2][2];
 
   const int ntiles = (key_hi - key_begin) / kBN + 1;
-  TileLoader<D> ld;
-  ld.init(rs, tid);
-  const int64_t tile_bytes = (int64_t)kBN * rs * 2;
-  const char *kt = (const char *)(kbase + (int64_t)key_begin * rs);
-  const char *vt = (const char *)(vbase + (int64_t)key_begin * rs);
-  ld.load(kt, vt, key_hi - key_begin + 1);
-  ld.store(sm, 0);
+  DmaTile<D, kBN> dma;
+  dma.init(tid, rs);
+  SwzOffsets so;
+  so.init(lane, D * 2);
+  const int64_t tile_elems = (int64_t)kBN * rs;
+  const bf16_t *kt = kbase + (int64_t)key_begin * rs;
+  const bf16_t *vt = vbase + (int64_t)key_begin * rs;
+  dma.issue(kt, rs, key_hi - key_begin + 1, sm.k[0]);
+  dma.issue(vt, rs, key_hi - key_begin + 1, sm.v[0]);
+  wait_vmem();
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
     const int c0 = key_begin + t * kBN;
     if (t + 1 < ntiles) {
-      kt += tile_bytes;
-      vt += tile_bytes;
-      ld.load(kt, vt, key_hi - (c0 + kBN) + 1);
+      kt += tile_elems;
+      vt += tile_elems;
+      dma.issue(kt, rs, key_hi - (c0 + kBN) + 1, sm.k[buf ^ 1]);
+      dma.issue(vt, rs, key_hi - (c0 + kBN) + 1, sm.v[buf ^ 1]);
     }
 
     if (active && c0 <= wave_hi) {
       // S^T[key][row] for two 32-key blocks
       f32x16 sacc[2][NQB];
+      const char *kl = (const char *)sm.k[buf];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const bf16_t *kp = &sm.k[buf][(kb * 32 + l32) * KSTR + hf * 8];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-          const bf16x8 kf = *(const bf16x8 *)(kp + ks * 16);
+          const bf16x8 kf = *(const bf16x8 *)(kl + kb * 32 * D * 2 + 128 * (ks >> 2) +
+                                              so.rowk[ks & 3]);
 #pragma unroll
           for (int qb = 0; qb < NQB; ++qb)
             sacc[kb][qb] = mfma32x32x16(kf, qf[qb][ks], ks == 0 ? f32x16{} : sacc[kb][qb]);
@@ -351,15 +266,16 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
       }
 
       // O^T[d][row] += V^T[d][key] P^T[key][row]
-      const char *vtb = (const char *)&sm.vt[buf][0];
+      const char *vl = (const char *)sm.v[buf];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
+        const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int bt = 0; bt < 2; ++bt) {
-            const bf16x8 vf =
-                *(const bf16x8 *)(vtb + vt_chunk(db * 32 + l32, kb, bt, hf));
+            const uint32_t o = cb + (kb * 32 + 16 * bt) * D * 2;
+            const bf16x8 vf = tr_operand_at(vl, o, o + 8 * D * 2);
 #pragma unroll
             for (int qb = 0; qb < NQB; ++qb)
               oacc[db][qb] = mfma32x32x16(vf, pf[qb][kb][bt], oacc[db][qb]);
@@ -367,7 +283,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
       }
     }
 
-    if (t + 1 < ntiles) ld.store(sm, buf ^ 1);
+    wait_vmem();
     __syncthreads();
   }
 
