@@ -80,24 +80,21 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 
 // ---------------------------------------------------------------- dK / dV
 
+// Q and dO tiles of 32 rows, unpadded swizzled rows (see swz()), filled by
+// direct global->LDS transfers; transposed operands are read with
+// ds_read_b64_tr_b16. Per-row LSE (log2), delta and lim ride along.
 template <int D>
 struct DkvSmem {
-  static constexpr int STR = D + 8;  // padded rows: conflict-free ds_read_b128
-  bf16_t q[2][kBR * STR];           // row-major; transposed operands come
-  bf16_t dout[2][kBR * STR];        // from ds_read_b64_tr_b16 (tr_operand)
-  float lse2[2][kBR];
-  float delta[2][kBR];
-  int lim[2][kBR];
+  bf16_t q[2][kBR * D];
+  bf16_t dout[2][kBR * D];
+  __attribute__((aligned(16))) float lse2[2][kBR];
+  __attribute__((aligned(16))) float delta[2][kBR];
+  __attribute__((aligned(16))) int lim[2][kBR];
 };
 
-// One 32-row tile of Q and dO, row-major, 16-byte chunks; threads 224..255
-// also stage the per-row LSE (as log2), delta and lim (lim = -1 marks rows
-// past the end of the dialogue).
-template <int D>
-struct RowTileLoader {
-  static constexpr int CPR = D / 8;              // chunks per row
-  static constexpr int CH = kBR * CPR / 256;     // chunks per thread per tensor
-  u32x4 rq[CH], rd[CH];
+// Threads 224..255 stage the per-row scalars of a 32-row tile (lim = -1
+// marks rows past the end of the dialogue).
+struct RowScalars {
   float l2, dl;
   int lm;
   bool has_row;
@@ -105,39 +102,21 @@ struct RowTileLoader {
   __device__ __forceinline__ void init(int tid) { has_row = tid >= 224; }
 
   __device__ __forceinline__ void load(const BwdArgs &a, int r0, int e, int h) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = min(r0 + c / CPR, e - 1), col = c % CPR;
-      const int64_t off = ((int64_t)row * a.hq + h) * D + col * 8;
-      rq[i] = *(const u32x4 *)((const bf16_t *)a.q + off);
-      rd[i] = *(const u32x4 *)((const bf16_t *)a.dout + off);
-    }
-    if (has_row) {
-      const int row = r0 + (threadIdx.x - 224);
-      const bool ok = row < e;
-      const int rc = ok ? row : e - 1;
-      l2 = a.lse[(int64_t)h * a.total + rc] * kLog2e;
-      dl = a.delta[(int64_t)h * a.total + rc];
-      lm = ok ? a.lim[rc] : -1;
-    }
+    if (!has_row) return;
+    const int row = r0 + ((int)threadIdx.x - 224);
+    const bool ok = row < e;
+    const int rc = ok ? row : e - 1;
+    l2 = a.lse[(int64_t)h * a.total + rc] * kLog2e;
+    dl = a.delta[(int64_t)h * a.total + rc];
+    lm = ok ? a.lim[rc] : -1;
   }
 
-  __device__ __forceinline__ void store(DkvSmem<D> &sm, int buf) {
-    constexpr int STR = DkvSmem<D>::STR;
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c / CPR, col = c % CPR;
-      *(u32x4 *)&sm.q[buf][row * STR + col * 8] = rq[i];
-      *(u32x4 *)&sm.dout[buf][row * STR + col * 8] = rd[i];
-    }
-    if (has_row) {
-      const int rr = threadIdx.x - 224;
-      sm.lse2[buf][rr] = l2;
-      sm.delta[buf][rr] = dl;
-      sm.lim[buf][rr] = lm;
-    }
+  __device__ __forceinline__ void store(float *lse2, float *delta, int *lim) const {
+    if (!has_row) return;
+    const int rr = (int)threadIdx.x - 224;
+    lse2[rr] = l2;
+    delta[rr] = dl;
+    lim[rr] = lm;
   }
 };
 
@@ -145,7 +124,7 @@ template <int D>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_DKV_WPE, ISM_DKV_WPE)))
 dkv_kernel(BwdArgs a, int ktiles) {
-  constexpr int NKS = D / 16, NDB = D / 32, STR = DkvSmem<D>::STR;
+  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2;
   __shared__ DkvSmem<D> sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, hf = lane >> 5;
@@ -185,10 +164,22 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int rstart = a.seer[c0];
   const int nrt = (e - rstart + kBR - 1) / kBR;
   const int iters = G * nrt;
-  RowTileLoader<D> ld;
-  ld.init(tid);
-  ld.load(a, rstart, e, kvh * G);
-  ld.store(sm, 0);
+  const int64_t rs = (int64_t)a.hq * D;
+  DmaTile<D, kBR> dma;
+  dma.init(tid, rs);
+  SwzOffsets so;
+  so.init(lane, RB);
+  RowScalars rsc;
+  rsc.init(tid);
+  auto issue = [&](int r0, int h, int buf) {
+    const int64_t base = ((int64_t)r0 * a.hq + h) * D;
+    dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[buf]);
+    dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[buf]);
+    rsc.load(a, r0, e, h);
+  };
+  issue(rstart, kvh * G, 0);
+  rsc.store(sm.lse2[0], sm.delta[0], sm.lim[0]);
+  wait_vmem();
   __syncthreads();
 
   for (int it = 0; it < iters; ++it) {
@@ -196,7 +187,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
     const int r0 = rstart + (it % nrt) * kBR;
     if (it + 1 < iters) {
       const int g1 = (it + 1) / nrt, rt1 = (it + 1) % nrt;
-      ld.load(a, rstart + rt1 * kBR, e, kvh * G + g1);
+      issue(rstart + rt1 * kBR, kvh * G + g1, buf ^ 1);
     }
     const int nvalid = min(kBR, e - r0);
     const int lim_last = sm.lim[buf][nvalid - 1];
@@ -204,12 +195,13 @@ dkv_kernel(BwdArgs a, int ktiles) {
       const bool full = nvalid == kBR && sm.lim[buf][0] >= kw0 + 31;
       // S[row][key] and dP[row][key], lane <-> key, rows 8i + 4hf + j
       f32x16 sacc, pacc;
-      const bf16_t *qp = &sm.q[buf][l32 * STR + hf * 8];
-      const bf16_t *dp = &sm.dout[buf][l32 * STR + hf * 8];
+      const char *ql = (const char *)sm.q[buf];
+      const char *dl = (const char *)sm.dout[buf];
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
-        sacc = mfma32x32x16(*(const bf16x8 *)(qp + ks * 16), kf[ks], ks == 0 ? f32x16{} : sacc);
-        pacc = mfma32x32x16(*(const bf16x8 *)(dp + ks * 16), vf[ks], ks == 0 ? f32x16{} : pacc);
+        const uint32_t o = 128 * (ks >> 2) + so.rowk[ks & 3];
+        sacc = mfma32x32x16(*(const bf16x8 *)(ql + o), kf[ks], ks == 0 ? f32x16{} : sacc);
+        pacc = mfma32x32x16(*(const bf16x8 *)(dl + o), vf[ks], ks == 0 ? f32x16{} : pacc);
       }
       const int key = kw0 + l32;
       bf16x8 pfr[2] = {}, dsf[2] = {};
@@ -244,16 +236,18 @@ dkv_kernel(BwdArgs a, int ktiles) {
       }
       // dV^T[d][key] += dO^T P, dK^T[d][key] += Q^T dS (contraction over rows)
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db) {
+        const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
 #pragma unroll
         for (int bt = 0; bt < 2; ++bt) {
-          dv[db] = mfma32x32x16(tr_operand(sm.dout[buf], STR, db * 32, 16 * bt, lane),
-                                pfr[bt], dv[db]);
-          dk[db] = mfma32x32x16(tr_operand(sm.q[buf], STR, db * 32, 16 * bt, lane),
-                                dsf[bt], dk[db]);
+          const uint32_t o = cb + 16 * bt * RB;
+          dv[db] = mfma32x32x16(tr_operand_at(dl, o, o + 8 * RB), pfr[bt], dv[db]);
+          dk[db] = mfma32x32x16(tr_operand_at(ql, o, o + 8 * RB), dsf[bt], dk[db]);
         }
+      }
     }
-    if (it + 1 < iters) ld.store(sm, buf ^ 1);
+    if (it + 1 < iters) rsc.store(sm.lse2[buf ^ 1], sm.delta[buf ^ 1], sm.lim[buf ^ 1]);
+    wait_vmem();
     __syncthreads();
   }
 
@@ -278,49 +272,19 @@ dkv_kernel(BwdArgs a, int ktiles) {
 
 // ---------------------------------------------------------------- dQ
 
+// K and V tiles of 64 keys, unpadded swizzled rows, double-buffered, filled
+// by direct global->LDS transfers; K^T is read through transposing reads.
 template <int D>
 struct DqSmem {
-  static constexpr int STR = D + 8;
-  bf16_t k[kBK * STR];   // row-major K tile: A operand of S^T = K Q^T, and
-                         // (through tr_operand) of dQ^T = K^T dS^T
-  bf16_t v[kBK * STR];   // row-major V tile: A operand of dP^T = V dO^T
-};
-
-// One 64-key tile of K and V, row-major 16-byte chunks.
-template <int D>
-struct KeyTileLoader {
-  static constexpr int CPR = D / 8;
-  static constexpr int CH = kBK * CPR / 256;
-  u32x4 kr[CH], vr[CH];
-
-  __device__ __forceinline__ void load(const bf16_t *kb, const bf16_t *vb, int64_t rs,
-                                       int c0, int key_hi) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int key = min(c0 + c / CPR, key_hi), col = c % CPR;
-      kr[i] = *(const u32x4 *)(kb + (int64_t)key * rs + col * 8);
-      vr[i] = *(const u32x4 *)(vb + (int64_t)key * rs + col * 8);
-    }
-  }
-
-  __device__ __forceinline__ void store(DqSmem<D> &sm) {
-    constexpr int STR = DqSmem<D>::STR;
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      const int row = c / CPR, col = c % CPR;
-      *(u32x4 *)&sm.k[row * STR + col * 8] = kr[i];
-      *(u32x4 *)&sm.v[row * STR + col * 8] = vr[i];
-    }
-  }
+  bf16_t k[2][kBK * D];
+  bf16_t v[2][kBK * D];
 };
 
 template <int D>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_DQ_WPE, ISM_DQ_WPE)))
 dq_kernel(BwdArgs a, int hpw, int tiles) {
-  constexpr int NKS = D / 16, NDB = D / 32, STR = DqSmem<D>::STR;
+  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2;
   __shared__ DqSmem<D> sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, hf = lane >> 5;
@@ -369,26 +333,40 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const bf16_t *vbase = (const bf16_t *)a.v + (int64_t)kvh * D;
   const int64_t rs = (int64_t)a.hkv * D;
   const int ntiles = (key_hi - s) / kBK + 1;
-  KeyTileLoader<D> ld;
-  ld.load(kbase, vbase, rs, s, key_hi);
+  DmaTile<D, kBK> dma;
+  dma.init(tid, rs);
+  SwzOffsets so;
+  so.init(lane, RB);
+  const int64_t tile_elems = (int64_t)kBK * rs;
+  const bf16_t *kt = kbase + (int64_t)s * rs;
+  const bf16_t *vt = vbase + (int64_t)s * rs;
+  dma.issue(kt, rs, key_hi - s + 1, sm.k[0]);
+  dma.issue(vt, rs, key_hi - s + 1, sm.v[0]);
+  wait_vmem();
+  __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
     const int c0 = s + t * kBK;
-    ld.store(sm);
-    __syncthreads();
-    if (t + 1 < ntiles) ld.load(kbase, vbase, rs, c0 + kBK, key_hi);
+    if (t + 1 < ntiles) {
+      kt += tile_elems;
+      vt += tile_elems;
+      dma.issue(kt, rs, key_hi - (c0 + kBK) + 1, sm.k[buf ^ 1]);
+      dma.issue(vt, rs, key_hi - (c0 + kBK) + 1, sm.v[buf ^ 1]);
+    }
     if (active && c0 <= wave_hi) {
       const bool full = c0 + kBK - 1 <= wave_lo;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         // S^T[key][row], dP^T[key][row] for 32 keys, lane <-> row
         f32x16 sacc, pacc;
-        const bf16_t *kp = &sm.k[(kb * 32 + l32) * STR + hf * 8];
-        const bf16_t *vp = &sm.v[(kb * 32 + l32) * STR + hf * 8];
+        const char *kl = (const char *)sm.k[buf];
+        const char *vl = (const char *)sm.v[buf];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-          sacc = mfma32x32x16(*(const bf16x8 *)(kp + ks * 16), qf[ks], ks == 0 ? f32x16{} : sacc);
-          pacc = mfma32x32x16(*(const bf16x8 *)(vp + ks * 16), df[ks], ks == 0 ? f32x16{} : pacc);
+          const uint32_t o = kb * 32 * RB + 128 * (ks >> 2) + so.rowk[ks & 3];
+          sacc = mfma32x32x16(*(const bf16x8 *)(kl + o), qf[ks], ks == 0 ? f32x16{} : sacc);
+          pacc = mfma32x32x16(*(const bf16x8 *)(vl + o), df[ks], ks == 0 ? f32x16{} : pacc);
         }
         bf16x8 dsf[2];
 #pragma unroll
@@ -410,13 +388,17 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
           dsf[bt] = __builtin_bit_cast(bf16x8, x);
         }
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
+        for (int db = 0; db < NDB; ++db) {
+          const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
 #pragma unroll
-          for (int bt = 0; bt < 2; ++bt)
-            dq[db] = mfma32x32x16(tr_operand(sm.k, STR, db * 32, kb * 32 + 16 * bt, lane),
-                                  dsf[bt], dq[db]);
+          for (int bt = 0; bt < 2; ++bt) {
+            const uint32_t o = cb + (kb * 32 + 16 * bt) * RB;
+            dq[db] = mfma32x32x16(tr_operand_at(kl, o, o + 8 * RB), dsf[bt], dq[db]);
+          }
+        }
       }
     }
+    wait_vmem();
     __syncthreads();
   }
 
