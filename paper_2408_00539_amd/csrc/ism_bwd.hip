@@ -22,7 +22,7 @@
 #include "ism_kernels.h"
 
 #ifndef ISM_DKV_WPE
-#define ISM_DKV_WPE 1
+#define ISM_DKV_WPE 2
 #endif
 #ifndef ISM_DQ_WPE
 #define ISM_DQ_WPE 2
@@ -52,11 +52,13 @@ bwd_prep_kernel(const int32_t *__restrict__ cu_segs,
   seer[j] = q ? cu_segs[lo] : j;
 }
 
-// delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads.
+// delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads; also the
+// LSE in log2 units (lse * log2 e) that the dK/dV kernel stages per tile.
 template <int D>
 __global__ void __launch_bounds__(256)
 delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
-             float *__restrict__ delta, int32_t total, int32_t hq) {
+             const float *__restrict__ lse, float *__restrict__ delta,
+             float *__restrict__ lse2, int32_t total, int32_t hq) {
   constexpr int LPR = D / 8;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t pairs = (int64_t)total * hq;
@@ -75,58 +77,68 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
   if (c == 0 && gid / LPR < pairs) {
     const int64_t row = rh / hq, h = rh % hq;
     delta[h * total + row] = acc;
+    lse2[h * total + row] = lse[h * total + row] * kLog2e;
   }
 }
 
 // ---------------------------------------------------------------- dK / dV
 
-// Q and dO tiles of 32 rows, unpadded swizzled rows (see swz()), filled by
-// direct global->LDS transfers; transposed operands are read with
-// ds_read_b64_tr_b16. Per-row LSE (log2), delta and lim ride along.
+constexpr int kDkvStages = 3;  // tiles in flight: compute one, two loading
+
+// Q and dO tiles of 32 rows (unpadded swizzled rows, see swz()) plus the
+// per-row LSE (log2 units), delta and lim, all filled by direct global->LDS
+// transfers, in a ring of kDkvStages buffers. Transposed operands are read
+// with ds_read_b64_tr_b16.
 template <int D>
 struct DkvSmem {
-  bf16_t q[2][kBR * D];
-  bf16_t dout[2][kBR * D];
-  __attribute__((aligned(16))) float lse2[2][kBR];
-  __attribute__((aligned(16))) float delta[2][kBR];
-  __attribute__((aligned(16))) int lim[2][kBR];
+  bf16_t q[kDkvStages][kBR * D];
+  bf16_t dout[kDkvStages][kBR * D];
+  __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
+  __attribute__((aligned(16))) float delta[kDkvStages][kBR];
+  __attribute__((aligned(16))) int lim[kDkvStages][kBR];
 };
 
-// Threads 224..255 stage the per-row scalars of a 32-row tile (lim = -1
-// marks rows past the end of the dialogue).
-struct RowScalars {
-  float l2, dl;
-  int lm;
-  bool has_row;
-
-  __device__ __forceinline__ void init(int tid) { has_row = tid >= 224; }
-
-  __device__ __forceinline__ void load(const BwdArgs &a, int r0, int e, int h) {
-    if (!has_row) return;
-    const int row = r0 + ((int)threadIdx.x - 224);
-    const bool ok = row < e;
-    const int rc = ok ? row : e - 1;
-    l2 = a.lse[(int64_t)h * a.total + rc] * kLog2e;
-    dl = a.delta[(int64_t)h * a.total + rc];
-    lm = ok ? a.lim[rc] : -1;
+// 32 consecutive 4-byte values base[min(r0 + l, last)], l < 32, to lds[l]
+// through one global_load_lds_dword (lanes 32..63 idle).
+__device__ __forceinline__ void dma_row_scalars(const void *base, int r0, int last, void *lds,
+                                                int lane) {
+  const uint32_t lb = lds_addr(lds);
+  if (lane < 32) {
+    const int r = min(r0 + lane, last);
+    dma_x1((const char *)base + (int64_t)r * 4, lb);
   }
+}
 
-  __device__ __forceinline__ void store(float *lse2, float *delta, int *lim) const {
-    if (!has_row) return;
-    const int rr = (int)threadIdx.x - 224;
-    lse2[rr] = l2;
-    delta[rr] = dl;
-    lim[rr] = lm;
+// s_waitcnt vmcnt(n) with expcnt / lgkmcnt left unconstrained.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<1>(); break;
+    case 2: wait_vmcnt<2>(); break;
+    default: wait_vmcnt<3>(); break;
   }
-};
+}
 
+// 8 waves: waves 0-3 accumulate dV and waves 4-7 dK for the same four
+// 32-key blocks, so that each wave holds one accumulator set (64 registers)
+// and two waves fit on every SIMD. Both roles recompute S (one extra GEMM in
+// five) in exchange for overlapping one role's exp/elementwise work with the
+// other's MFMAs.
 template <int D>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(ISM_DKV_WPE, ISM_DKV_WPE)))
 dkv_kernel(BwdArgs a, int ktiles) {
   constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2;
   __shared__ DkvSmem<D> sm;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kblk = wave & 3, role = wave >> 2;  // role 0: dV, role 1: dK
   const int l32 = lane & 31, hf = lane >> 5;
 
   // (dialogue, KV head) groups run on one XCD each; early key tiles (the
@@ -140,7 +152,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int s = a.cu_seqlens[b], e = a.cu_seqlens[b + 1];
   const int c0 = s + kt * kKW;
   if (c0 >= e) return;
-  const int kw0 = c0 + 32 * wave;
+  const int kw0 = c0 + 32 * kblk;
   const bool wactive = kw0 < e;
   const int G = a.hq / a.hkv;
   const float sl2 = a.scale * kLog2e;
@@ -154,119 +166,171 @@ dkv_kernel(BwdArgs a, int ktiles) {
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       kf[ks] = *(const bf16x8 *)(kp + ks * 16);
-      vf[ks] = *(const bf16x8 *)(vp + ks * 16);
+      vf[ks] = role ? *(const bf16x8 *)(vp + ks * 16) : bf16x8{};
     }
+    wait_loads();
   }
-  f32x16 dk[NDB], dv[NDB];
+  f32x16 acc[NDB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) { dk[db] = f32x16{}; dv[db] = f32x16{}; }
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
 
   const int rstart = a.seer[c0];
   const int nrt = (e - rstart + kBR - 1) / kBR;
   const int iters = G * nrt;
   const int64_t rs = (int64_t)a.hq * D;
-  DmaTile<D, kBR> dma;
+  DmaTile<D, kBR, 8> dma;
   dma.init(tid, rs);
   SwzOffsets so;
   so.init(lane, RB);
-  RowScalars rsc;
-  rsc.init(tid);
-  auto issue = [&](int r0, int h, int buf) {
-    const int64_t base = ((int64_t)r0 * a.hq + h) * D;
-    dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[buf]);
-    dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[buf]);
-    rsc.load(a, r0, e, h);
+  // transfers this wave issues per tile: Q and dO blocks, plus one row-scalar
+  // array for waves 5, 6, 7
+  const int my_ops = 2 * (wave < DmaTile<D, kBR, 8>::T ? 1 : 0) + (wave >= 5 ? 1 : 0);
+  // Sources of tile t: Q and dO rows, and the per-row scalars of its head.
+  struct TileSrc {
+    const bf16_t *q, *d;
+    const float *l, *dl;
+    int r0;
   };
-  issue(rstart, kvh * G, 0);
-  rsc.store(sm.lse2[0], sm.delta[0], sm.lim[0]);
-  wait_vmem();
-  __syncthreads();
-
-  for (int it = 0; it < iters; ++it) {
-    const int buf = it & 1;
-    const int r0 = rstart + (it % nrt) * kBR;
-    if (it + 1 < iters) {
-      const int g1 = (it + 1) / nrt, rt1 = (it + 1) % nrt;
-      issue(rstart + rt1 * kBR, kvh * G + g1, buf ^ 1);
+  auto tile_src = [&](int t) {
+    const int h = kvh * G + t / nrt, r0 = rstart + (t % nrt) * kBR;
+    const int64_t base = ((int64_t)r0 * a.hq + h) * D;
+    return TileSrc{(const bf16_t *)a.q + base, (const bf16_t *)a.dout + base,
+                   a.lse2 + (int64_t)h * a.total, a.delta + (int64_t)h * a.total, r0};
+  };
+  // Transfers of one tile into one stage of the ring. All pointers are
+  // __restrict__ so that, once inlined, the transfers carry alias scopes.
+  auto issue = [&](const bf16_t *__restrict__ gq, const bf16_t *__restrict__ gd,
+                   const float *__restrict__ gl, const float *__restrict__ gdl,
+                   const int *__restrict__ glim, int r0, bf16_t *__restrict__ q_n,
+                   bf16_t *__restrict__ d_n, float *__restrict__ l_n,
+                   float *__restrict__ dl_n, int *__restrict__ lim_n) {
+    dma.issue(gq, rs, e - r0, q_n);
+    dma.issue(gd, rs, e - r0, d_n);
+    if (wave == 5) dma_row_scalars(gl, r0, e - 1, l_n, lane);
+    if (wave == 6) dma_row_scalars(gdl, r0, e - 1, dl_n, lane);
+    if (wave == 7) dma_row_scalars(glim, r0, e - 1, lim_n, lane);
+  };
+#pragma unroll
+  for (int t = 0; t < kDkvStages - 1; ++t)
+    if (t < iters) {
+      const TileSrc ts = tile_src(t);
+      issue(ts.q, ts.d, ts.l, ts.dl, a.lim, ts.r0, sm.q[t], sm.dout[t], sm.lse2[t],
+            sm.delta[t], sm.lim[t]);
     }
+
+  // One step: start the transfers of a later tile into the free stage (the
+  // *_n buffers, sources g*) and compute on the current stage (*_c). The
+  // __restrict__ qualifiers tell the compiler the stages never overlap, so
+  // it does not make the current stage's LDS reads wait for the new
+  // transfers.
+  auto step = [&](const bf16_t *__restrict__ q_c, const bf16_t *__restrict__ d_c,
+                  const float *__restrict__ l_c, const float *__restrict__ dl_c,
+                  const int *__restrict__ lim_c, bf16_t *__restrict__ q_n,
+                  bf16_t *__restrict__ d_n, float *__restrict__ l_n, float *__restrict__ dl_n,
+                  int *__restrict__ lim_n, const bf16_t *__restrict__ gq,
+                  const bf16_t *__restrict__ gd, const float *__restrict__ gl,
+                  const float *__restrict__ gdl, const int *__restrict__ glim, int rn,
+                  bool more, int r0) {
+    if (more) issue(gq, gd, gl, gdl, glim, rn, q_n, d_n, l_n, dl_n, lim_n);
     const int nvalid = min(kBR, e - r0);
-    const int lim_last = sm.lim[buf][nvalid - 1];
-    if (wactive && lim_last >= kw0) {
-      const bool full = nvalid == kBR && sm.lim[buf][0] >= kw0 + 31;
-      // S[row][key] and dP[row][key], lane <-> key, rows 8i + 4hf + j
-      f32x16 sacc, pacc;
-      const char *ql = (const char *)sm.q[buf];
-      const char *dl = (const char *)sm.dout[buf];
+    const int lim_last = lim_c[nvalid - 1];
+    if (!wactive || lim_last < kw0) return;
+    // rows at or past nvalid repeat the last row (clamped transfers) and
+    // are masked in the partial path
+    const bool full = nvalid == kBR && lim_c[0] >= kw0 + 31;
+    const char *ql = (const char *)q_c;
+    const char *dl = (const char *)d_c;
+    const int key = kw0 + l32;
+    // S[row][key] (lane <-> key, rows 8i + 4hf + j); role 1 also dP
+    f32x16 sacc, pacc;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const uint32_t o = 128 * (ks >> 2) + so.rowk[ks & 3];
+      sacc = mfma32x32x16(*(const bf16x8 *)(ql + o), kf[ks], ks == 0 ? f32x16{} : sacc);
+    }
+    if (role) {
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         const uint32_t o = 128 * (ks >> 2) + so.rowk[ks & 3];
-        sacc = mfma32x32x16(*(const bf16x8 *)(ql + o), kf[ks], ks == 0 ? f32x16{} : sacc);
         pacc = mfma32x32x16(*(const bf16x8 *)(dl + o), vf[ks], ks == 0 ? f32x16{} : pacc);
       }
-      const int key = kw0 + l32;
-      bf16x8 pfr[2] = {}, dsf[2] = {};
+    }
+    // P = exp(S - LSE) (masked); role 1: dS = P (dP - delta)
+    bf16x8 fr[2] = {};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const f32x4 l2 = *(const f32x4 *)&sm.lse2[buf][8 * i + 4 * hf];
-        const f32x4 dl = *(const f32x4 *)&sm.delta[buf][8 * i + 4 * hf];
-        int lm[4] = {0, 0, 0, 0};
-        if (!full) {
-          const u32x4 li = *(const u32x4 *)&sm.lim[buf][8 * i + 4 * hf];
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 l2 = *(const f32x4 *)&l_c[8 * i + 4 * hf];
+      int lm[4] = {0, 0, 0, 0};
+      if (!full) {
+        const u32x4 li = *(const u32x4 *)&lim_c[8 * i + 4 * hf];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) lm[j] = (int)li[j];
-        }
-        f32x2 pp[2], dd[2];
+        for (int j = 0; j < 4; ++j) lm[j] = (8 * i + 4 * hf + j < nvalid) ? (int)li[j] : -1;
+      }
+      f32x2 w[2];
+      if (role) {
+        const f32x4 dlt = *(const f32x4 *)&dl_c[8 * i + 4 * hf];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           float p = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
           if (!full && key > lm[j]) p = 0.f;
-          pp[j >> 1][j & 1] = p;
-          dd[j >> 1][j & 1] = p * (pacc[4 * i + j] - dl[j]);
+          w[j >> 1][j & 1] = p * (pacc[4 * i + j] - dlt[j]);
         }
-        // rows 8i..8i+3 (+4hf) are slots 4*(i&1).. of operand i>>1
-        const int bt = i >> 1, sl = (i & 1) * 2;
-        u32x4 wp = __builtin_bit_cast(u32x4, pfr[bt]);
-        u32x4 wd = __builtin_bit_cast(u32x4, dsf[bt]);
-        wp[sl] = cvt_bf16x2(pp[0]);
-        wp[sl + 1] = cvt_bf16x2(pp[1]);
-        wd[sl] = cvt_bf16x2(dd[0]);
-        wd[sl + 1] = cvt_bf16x2(dd[1]);
-        pfr[bt] = __builtin_bit_cast(bf16x8, wp);
-        dsf[bt] = __builtin_bit_cast(bf16x8, wd);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float p = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
+          if (!full && key > lm[j]) p = 0.f;
+          w[j >> 1][j & 1] = p;
+        }
       }
-      // dV^T[d][key] += dO^T P, dK^T[d][key] += Q^T dS (contraction over rows)
+      // rows 8i..8i+3 (+4hf) are slots 4*(i&1).. of operand i>>1
+      const int bt = i >> 1, sl = (i & 1) * 2;
+      u32x4 x = __builtin_bit_cast(u32x4, fr[bt]);
+      x[sl] = cvt_bf16x2(w[0]);
+      x[sl + 1] = cvt_bf16x2(w[1]);
+      fr[bt] = __builtin_bit_cast(bf16x8, x);
+    }
+    // role 0: dV^T[d][key] += dO^T P; role 1: dK^T[d][key] += Q^T dS
+    const char *src = role ? ql : dl;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
+    for (int db = 0; db < NDB; ++db) {
+      const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
 #pragma unroll
-        for (int bt = 0; bt < 2; ++bt) {
-          const uint32_t o = cb + 16 * bt * RB;
-          dv[db] = mfma32x32x16(tr_operand_at(dl, o, o + 8 * RB), pfr[bt], dv[db]);
-          dk[db] = mfma32x32x16(tr_operand_at(ql, o, o + 8 * RB), dsf[bt], dk[db]);
-        }
+      for (int bt = 0; bt < 2; ++bt) {
+        const uint32_t o = cb + 16 * bt * RB;
+        acc[db] = mfma32x32x16(tr_operand_at(src, o, o + 8 * RB), fr[bt], acc[db]);
       }
     }
-    if (it + 1 < iters) rsc.store(sm.lse2[buf ^ 1], sm.delta[buf ^ 1], sm.lim[buf ^ 1]);
-    wait_vmem();
-    __syncthreads();
+  };
+
+  for (int it = 0; it < iters; ++it) {
+    const int buf = it % kDkvStages, nb = (it + kDkvStages - 1) % kDkvStages;
+    const int r0 = rstart + (it % nrt) * kBR;
+    // tile it has landed once at most the next tile's transfers are pending
+    if (it + 1 < iters) wait_vmcnt_dyn(my_ops); else wait_vmcnt<0>();
+    // Tile it visible to all waves, and every wave is done reading tile
+    // it - 1 (its reads were consumed by MFMAs). A bare s_barrier: the fences
+    // of __syncthreads() would also drain the transfers still in flight.
+    lds_barrier();
+    const int tn = it + kDkvStages - 1;
+    const TileSrc ts = tile_src(tn < iters ? tn : it);
+    step(sm.q[buf], sm.dout[buf], sm.lse2[buf], sm.delta[buf], sm.lim[buf], sm.q[nb],
+         sm.dout[nb], sm.lse2[nb], sm.delta[nb], sm.lim[nb], ts.q, ts.d, ts.l, ts.dl, a.lim,
+         ts.r0, tn < iters, r0);
   }
 
   const int key = kw0 + l32;
   if (!wactive || key >= e) return;
-  float *dkp = a.dk + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
-  float *dvp = a.dv + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
+  float *out = (role ? a.dk : a.dv) + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
+  const float mul = role ? a.scale : 1.f;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      f32x4 xk, xv;
+      f32x4 x;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        xk[j] = dk[db][4 * i + j] * a.scale;
-        xv[j] = dv[db][4 * i + j];
-      }
-      *(f32x4 *)(dkp + db * 32 + 8 * i) = xk;
-      *(f32x4 *)(dvp + db * 32 + 8 * i) = xv;
+      for (int j = 0; j < 4; ++j) x[j] = acc[db][4 * i + j] * mul;
+      *(f32x4 *)(out + db * 32 + 8 * i) = x;
     }
 }
 
@@ -313,7 +377,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
 
   const int rc = min(wq0 + l32, e - 1);
   const int lim_r = a.lim[rc];
-  const float lse2 = a.lse[(int64_t)head * a.total + rc] * kLog2e;
+  const float lse2 = a.lse2[(int64_t)head * a.total + rc];
   const float dlt = a.delta[(int64_t)head * a.total + rc];
   bf16x8 qf[NKS], df[NKS];
   {
@@ -324,6 +388,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       qf[ks] = *(const bf16x8 *)(qp + ks * 16);
       df[ks] = *(const bf16x8 *)(dp + ks * 16);
     }
+    wait_loads();
   }
   f32x16 dq[NDB];
 #pragma unroll
@@ -426,14 +491,14 @@ hipError_t launch_bwd_t(const BwdArgs &a, hipStream_t stream) {
   const int64_t pairs = (int64_t)a.total * a.hq;
   const int64_t thr = pairs * (D / 8);
   hipLaunchKernelGGL((delta_kernel<D>), dim3((unsigned)((thr + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t *)a.o, (const bf16_t *)a.dout, a.delta, a.total,
-                     a.hq);
+                     stream, (const bf16_t *)a.o, (const bf16_t *)a.dout, a.lse, a.delta,
+                     a.lse2, a.total, a.hq);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
 
   const int ktiles = (a.max_seqlen + kKW - 1) / kKW;
   const int64_t tot_kv = (int64_t)a.batch * a.hkv * ktiles;
-  hipLaunchKernelGGL((dkv_kernel<D>), dim3((unsigned)(8 * ((tot_kv + 7) / 8))), dim3(256), 0,
+  hipLaunchKernelGGL((dkv_kernel<D>), dim3((unsigned)(8 * ((tot_kv + 7) / 8))), dim3(512), 0,
                      stream, a, ktiles);
   if ((err = hipGetLastError()) != hipSuccess) return err;
 

@@ -91,20 +91,62 @@ __device__ __forceinline__ bf16x8 tr_operand(const bf16_t *tile, int str, int m0
 // and for the 4 consecutive rows x 32 bytes of a ds_read_b64_tr_b16 group.
 __device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
 
+// Byte address of a pointer into LDS.
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// global_load_lds_dwordx4 / _dword: each active lane copies 16 / 4 bytes
+// from its global address to LDS at lds_base + 16 * lane / 4 * lane
+// (lds_base wave-uniform, placed in M0). Written as inline assembly so that
+// the compiler does not model the LDS write: the kernels order these
+// transfers themselves with counted s_waitcnt vmcnt and barriers, and the
+// compiler would otherwise drain every transfer in flight before each LDS
+// read of another buffer.
+__device__ __forceinline__ void dma_x4(const void *g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_x1(const void *g, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+               : "memory", "m0");
+}
+
+// Workgroup barrier without memory fences, for loops that order their LDS
+// traffic with explicit s_waitcnt: outstanding LDS reads are drained first,
+// global->LDS transfers are left in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+}
+
+// Compiler-visible wait for all outstanding vector-memory loads of this
+// wave (register operands loaded before a pipelined loop), so that the
+// compiler's own wait accounting does not carry them into the loop.
+__device__ __forceinline__ void wait_loads() {
+  __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));
+}
+
 // Wait until this wave's outstanding vector-memory operations, including
 // global->LDS transfers, have completed.
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Direct global->LDS staging of a ROWS x D bf16 tile (unpadded, swizzled)
-// by the 4 waves of a workgroup. Each global_load_lds_dwordx4 writes lane l's
-// 16 bytes to LDS bytes [16 l, 16 l + 16) of a 1 KB block, so the swizzle is
-// applied by choosing each lane's source chunk. No registers hold the data.
-template <int D, int ROWS>
+// by the NW waves of a workgroup. Each global_load_lds_dwordx4 writes lane
+// l's 16 bytes to LDS bytes [16 l, 16 l + 16) of a 1 KB block, so the swizzle
+// is applied by choosing each lane's source chunk. No registers hold the
+// data. Block q of the tile is issued by wave q % NW.
+template <int D, int ROWS, int NW = 4>
 struct DmaTile {
-  static constexpr int CPR = D / 8;          // 16-byte chunks per row
-  static constexpr int RPI = 64 / CPR;       // rows per 1 KB transfer
-  static constexpr int NI = ROWS / RPI / 4;  // transfers per wave
-  static_assert(NI >= 1 && ROWS % (4 * RPI) == 0, "tile not divisible among 4 waves");
+  static constexpr int CPR = D / 8;                 // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;              // rows per 1 KB transfer
+  static constexpr int T = ROWS / RPI;              // transfers per tile
+  static constexpr int NI = (T + NW - 1) / NW;      // transfers per wave (max)
+  static_assert(ROWS % RPI == 0, "tile rows must fill whole transfers");
   uint32_t loff[NI];  // element offset of this lane's source chunk (full tile)
   int wave, lane;
 
@@ -113,7 +155,7 @@ struct DmaTile {
     lane = tid & 63;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int r = (wave * NI + i) * RPI + lane / CPR;
+      const int r = (i * NW + wave) * RPI + lane / CPR;
       loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz(r)) * 8);
     }
   }
@@ -122,20 +164,21 @@ struct DmaTile {
   // at or past nvalid repeat row nvalid - 1 (always valid memory).
   __device__ __forceinline__ void issue(const bf16_t *src, int64_t rs, int nvalid,
                                         bf16_t *lds) const {
-    typedef __attribute__((address_space(3))) void lds_void;
+    const uint32_t lb = lds_addr(lds);
     if (__builtin_amdgcn_readfirstlane(nvalid) >= ROWS) {
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
-        __builtin_amdgcn_global_load_lds((const void *)(src + loff[i]),
-                                         (lds_void *)(lds + (wave * NI + i) * 512), 16, 0, 0);
+      for (int i = 0; i < NI; ++i) {
+        const int q = i * NW + wave;
+        if (q < T) dma_x4(src + loff[i], lb + q * 1024);
+      }
     } else {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        const int r = (wave * NI + i) * RPI + lane / CPR;
+        const int q = i * NW + wave;
+        if (q >= T) continue;
+        const int r = q * RPI + lane / CPR;
         const int rr = min(r, nvalid - 1);
-        const bf16_t *g = src + (int64_t)rr * rs + ((lane % CPR) ^ swz(r)) * 8;
-        __builtin_amdgcn_global_load_lds((const void *)g,
-                                         (lds_void *)(lds + (wave * NI + i) * 512), 16, 0, 0);
+        dma_x4(src + (int64_t)rr * rs + ((lane % CPR) ^ swz(r)) * 8, lb + q * 1024);
       }
     }
   }

@@ -202,6 +202,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[qb][ks] = *(const bf16x8 *)(qp + ks * 16);
   }
+  wait_loads();
 
   f32x16 oacc[NDB][NQB];
 #pragma unroll
