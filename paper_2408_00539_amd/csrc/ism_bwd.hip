@@ -8,12 +8,11 @@
 //     non-decreasing inside a dialogue and lim(j) >= j).
 //  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji).
 //  3. dK/dV kernel, key-tile outer: a workgroup owns 128 keys of one KV head
-//     (32 per wave, lane <-> key), walks the query heads of the group and the
-//     32-row tiles from seer[first key] to the dialogue end, and accumulates
-//     dV^T += dO^T P and dK^T += Q^T dS with P = exp(S - LSE),
+//     (32 per wave pair, lane <-> key), walks the query heads of the group
+//     and the 32-row tiles from seer[first key] to the dialogue end, and
+//     accumulates dV^T += dO^T P and dK^T += Q^T dS with P = exp(S - LSE),
 //     dS = P o (dP - delta), dP = dO V^T. Q and dO tiles are staged in LDS
-//     both row-major (for S and dP) and transposed (for the two products
-//     over rows).
+//     row-major; the products over rows read them through transposing reads.
 //  4. dQ kernel, row-tile outer like the forward (lane <-> row): recomputes
 //     S^T and dP^T per 64-key tile and accumulates dQ^T += K^T dS^T.
 // All products are bf16 MFMA 32x32x16 with fp32 accumulation; gradients are
@@ -83,12 +82,15 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 
 // ---------------------------------------------------------------- dK / dV
 
-constexpr int kDkvStages = 3;  // tiles in flight: compute one, two loading
+// Ring of Q / dO tile stages: the tile a dS wave finishes (t - 1), the
+// current tile t, and tiles t + 1, t + 2 in flight.
+constexpr int kDkvStages = 4;
 
-// Q and dO tiles of 32 rows (unpadded swizzled rows, see swz()) plus the
+// Q and dO tiles of 32 rows (unpadded swizzled rows, see swz<D>()) plus the
 // per-row LSE (log2 units), delta and lim, all filled by direct global->LDS
-// transfers, in a ring of kDkvStages buffers. Transposed operands are read
-// with ds_read_b64_tr_b16.
+// transfers; and P of the last two tiles for each wave pair, fp32 in MFMA
+// accumulator layout (lane-private, 16 values per lane, stored as 4 x 16
+// bytes so that consecutive lanes touch consecutive bytes).
 template <int D>
 struct DkvSmem {
   bf16_t q[kDkvStages][kBR * D];
@@ -96,6 +98,7 @@ struct DkvSmem {
   __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
   __attribute__((aligned(16))) float delta[kDkvStages][kBR];
   __attribute__((aligned(16))) int lim[kDkvStages][kBR];
+  __attribute__((aligned(16))) float p[2][4][16 * 64];
 };
 
 // 32 consecutive 4-byte values base[min(r0 + l, last)], l < 32, to lds[l]
@@ -125,11 +128,27 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
   }
 }
 
-// 8 waves: waves 0-3 accumulate dV and waves 4-7 dK for the same four
-// 32-key blocks, so that each wave holds one accumulator set (64 registers)
-// and two waves fit on every SIMD. Both roles recompute S (one extra GEMM in
-// five) in exchange for overlapping one role's exp/elementwise work with the
-// other's MFMAs.
+// fr[bt] slots of the B operand (16 rows x 32 keys) from four accumulator
+// rows groups: accumulator rows 8i..8i+3 (+4 for the upper half-wave) are
+// slots 4 (i & 1) .. of operand i >> 1, matching the k order of the
+// transposing A-operand reads.
+__device__ __forceinline__ void put_rows(bf16x8 (&fr)[2], int i, f32x2 lo, f32x2 hi) {
+  const int bt = i >> 1, sl = (i & 1) * 2;
+  u32x4 x = __builtin_bit_cast(u32x4, fr[bt]);
+  x[sl] = cvt_bf16x2(lo);
+  x[sl + 1] = cvt_bf16x2(hi);
+  fr[bt] = __builtin_bit_cast(bf16x8, x);
+}
+
+// Eight waves in four pairs; pair p owns the 32 keys c0 + 32 p (lane <->
+// key) and its two waves share one SIMD:
+//  * the P wave (p) computes S = Q K^T and P = exp(S - LSE) (masked) for
+//    tile t, accumulates dV^T += dO^T P and leaves P in LDS;
+//  * the dS wave (p + 4) computes dP = dO V^T for tile t and, one tile
+//    behind, dS = P o (dP - delta) with its partner's P, dK^T += Q^T dS.
+// Each wave does 16 of the 32 products per tile with no product computed
+// twice, and the exp / elementwise phase of one wave of a pair falls in the
+// other's MFMA phase.
 template <int D>
 __global__ void __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(ISM_DKV_WPE, ISM_DKV_WPE)))
@@ -138,7 +157,8 @@ dkv_kernel(BwdArgs a, int ktiles) {
   __shared__ DkvSmem<D> sm;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int kblk = wave & 3, role = wave >> 2;  // role 0: dV, role 1: dK
+  const int pair = wave & 3;
+  const bool pwave = wave < 4;
   const int l32 = lane & 31, hf = lane >> 5;
 
   // (dialogue, KV head) groups run on one XCD each; early key tiles (the
@@ -152,27 +172,27 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int s = a.cu_seqlens[b], e = a.cu_seqlens[b + 1];
   const int c0 = s + kt * kKW;
   if (c0 >= e) return;
-  const int kw0 = c0 + 32 * kblk;
+  const int kw0 = c0 + 32 * pair;
   const bool wactive = kw0 < e;
   const int G = a.hq / a.hkv;
   const float sl2 = a.scale * kLog2e;
 
-  // this wave's 32 keys as B operands (lane <-> key, 8 head-dim values)
-  bf16x8 kf[NKS], vf[NKS];
+  // B operands of this wave's products: K (P wave, for S) or V (dS wave,
+  // for dP) of its 32 keys, lane <-> key, 8 head-dim values per k step
+  bf16x8 bop[NKS];
   {
     const int key = min(kw0 + l32, e - 1);
-    const bf16_t *kp = (const bf16_t *)a.k + ((int64_t)key * a.hkv + kvh) * D + hf * 8;
-    const bf16_t *vp = (const bf16_t *)a.v + ((int64_t)key * a.hkv + kvh) * D + hf * 8;
+    const bf16_t *src =
+        (const bf16_t *)(pwave ? a.k : a.v) + ((int64_t)key * a.hkv + kvh) * D + hf * 8;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      kf[ks] = *(const bf16x8 *)(kp + ks * 16);
-      vf[ks] = role ? *(const bf16x8 *)(vp + ks * 16) : bf16x8{};
-    }
+    for (int ks = 0; ks < NKS; ++ks) bop[ks] = *(const bf16x8 *)(src + ks * 16);
     wait_loads();
   }
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  f32x16 dp = {};        // dS wave: dP of the previous tile
+  bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   const int rstart = a.seer[c0];
   const int nrt = (e - rstart + kBR - 1) / kBR;
@@ -180,149 +200,123 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int64_t rs = (int64_t)a.hq * D;
   DmaTile<D, kBR, 8> dma;
   dma.init(tid, rs);
-  SwzOffsets so;
-  so.init(lane, RB);
+  SwzOffsets<D> so;
+  so.init(lane);
   // transfers this wave issues per tile: Q and dO blocks, plus one row-scalar
   // array for waves 5, 6, 7
   const int my_ops = 2 * (wave < DmaTile<D, kBR, 8>::T ? 1 : 0) + (wave >= 5 ? 1 : 0);
-  // Sources of tile t: Q and dO rows, and the per-row scalars of its head.
-  struct TileSrc {
-    const bf16_t *q, *d;
-    const float *l, *dl;
-    int r0;
-  };
-  auto tile_src = [&](int t) {
+  auto issue = [&](int t) {
+    const int st = t % kDkvStages;
     const int h = kvh * G + t / nrt, r0 = rstart + (t % nrt) * kBR;
     const int64_t base = ((int64_t)r0 * a.hq + h) * D;
-    return TileSrc{(const bf16_t *)a.q + base, (const bf16_t *)a.dout + base,
-                   a.lse2 + (int64_t)h * a.total, a.delta + (int64_t)h * a.total, r0};
+    dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[st]);
+    dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[st]);
+    if (wave == 5) dma_row_scalars(a.lse2 + (int64_t)h * a.total, r0, e - 1, sm.lse2[st], lane);
+    if (wave == 6) dma_row_scalars(a.delta + (int64_t)h * a.total, r0, e - 1, sm.delta[st], lane);
+    if (wave == 7) dma_row_scalars(a.lim, r0, e - 1, sm.lim[st], lane);
   };
-  // Transfers of one tile into one stage of the ring. All pointers are
-  // __restrict__ so that, once inlined, the transfers carry alias scopes.
-  auto issue = [&](const bf16_t *__restrict__ gq, const bf16_t *__restrict__ gd,
-                   const float *__restrict__ gl, const float *__restrict__ gdl,
-                   const int *__restrict__ glim, int r0, bf16_t *__restrict__ q_n,
-                   bf16_t *__restrict__ d_n, float *__restrict__ l_n,
-                   float *__restrict__ dl_n, int *__restrict__ lim_n) {
-    dma.issue(gq, rs, e - r0, q_n);
-    dma.issue(gd, rs, e - r0, d_n);
-    if (wave == 5) dma_row_scalars(gl, r0, e - 1, l_n, lane);
-    if (wave == 6) dma_row_scalars(gdl, r0, e - 1, dl_n, lane);
-    if (wave == 7) dma_row_scalars(glim, r0, e - 1, lim_n, lane);
-  };
-#pragma unroll
-  for (int t = 0; t < kDkvStages - 1; ++t)
-    if (t < iters) {
-      const TileSrc ts = tile_src(t);
-      issue(ts.q, ts.d, ts.l, ts.dl, a.lim, ts.r0, sm.q[t], sm.dout[t], sm.lse2[t],
-            sm.delta[t], sm.lim[t]);
-    }
 
-  // One step: start the transfers of a later tile into the free stage (the
-  // *_n buffers, sources g*) and compute on the current stage (*_c). The
-  // __restrict__ qualifiers tell the compiler the stages never overlap, so
-  // it does not make the current stage's LDS reads wait for the new
-  // transfers.
-  auto step = [&](const bf16_t *__restrict__ q_c, const bf16_t *__restrict__ d_c,
-                  const float *__restrict__ l_c, const float *__restrict__ dl_c,
-                  const int *__restrict__ lim_c, bf16_t *__restrict__ q_n,
-                  bf16_t *__restrict__ d_n, float *__restrict__ l_n, float *__restrict__ dl_n,
-                  int *__restrict__ lim_n, const bf16_t *__restrict__ gq,
-                  const bf16_t *__restrict__ gd, const float *__restrict__ gl,
-                  const float *__restrict__ gdl, const int *__restrict__ glim, int rn,
-                  bool more, int r0) {
-    if (more) issue(gq, gd, gl, gdl, glim, rn, q_n, d_n, l_n, dl_n, lim_n);
-    const int nvalid = min(kBR, e - r0);
-    const int lim_last = lim_c[nvalid - 1];
-    if (!wactive || lim_last < kw0) return;
-    // rows at or past nvalid repeat the last row (clamped transfers) and
-    // are masked in the partial path
-    const bool full = nvalid == kBR && lim_c[0] >= kw0 + 31;
-    const char *ql = (const char *)q_c;
-    const char *dl = (const char *)d_c;
-    const int key = kw0 + l32;
-    // S[row][key] (lane <-> key, rows 8i + 4hf + j); role 1 also dP
-    f32x16 sacc, pacc;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) {
-      const uint32_t o = 128 * (ks >> 2) + so.rowk[ks & 3];
-      sacc = mfma32x32x16(*(const bf16x8 *)(ql + o), kf[ks], ks == 0 ? f32x16{} : sacc);
-    }
-    if (role) {
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const uint32_t o = 128 * (ks >> 2) + so.rowk[ks & 3];
-        pacc = mfma32x32x16(*(const bf16x8 *)(dl + o), vf[ks], ks == 0 ? f32x16{} : pacc);
-      }
-    }
-    // P = exp(S - LSE) (masked); role 1: dS = P (dP - delta)
+  // dS wave: dS = P o (dP - delta) for the tile in stage sp (P from pbuf),
+  // then dK^T[d][key] += Q^T[d][row] dS[row][key].
+  auto ds_step = [&](int sp, int pbuf) {
+    const float *pp = sm.p[pbuf][pair];
     bf16x8 fr[2] = {};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const f32x4 l2 = *(const f32x4 *)&l_c[8 * i + 4 * hf];
-      int lm[4] = {0, 0, 0, 0};
-      if (!full) {
-        const u32x4 li = *(const u32x4 *)&lim_c[8 * i + 4 * hf];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) lm[j] = (8 * i + 4 * hf + j < nvalid) ? (int)li[j] : -1;
-      }
+      const f32x4 pv = *(const f32x4 *)(pp + (i * 64 + lane) * 4);
+      const f32x4 dlt = *(const f32x4 *)&sm.delta[sp][8 * i + 4 * hf];
       f32x2 w[2];
-      if (role) {
-        const f32x4 dlt = *(const f32x4 *)&dl_c[8 * i + 4 * hf];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float p = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
-          if (!full && key > lm[j]) p = 0.f;
-          w[j >> 1][j & 1] = p * (pacc[4 * i + j] - dlt[j]);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float p = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
-          if (!full && key > lm[j]) p = 0.f;
-          w[j >> 1][j & 1] = p;
-        }
-      }
-      // rows 8i..8i+3 (+4hf) are slots 4*(i&1).. of operand i>>1
-      const int bt = i >> 1, sl = (i & 1) * 2;
-      u32x4 x = __builtin_bit_cast(u32x4, fr[bt]);
-      x[sl] = cvt_bf16x2(w[0]);
-      x[sl + 1] = cvt_bf16x2(w[1]);
-      fr[bt] = __builtin_bit_cast(bf16x8, x);
+      for (int j = 0; j < 4; ++j) w[j >> 1][j & 1] = pv[j] * (dp[4 * i + j] - dlt[j]);
+      put_rows(fr, i, w[0], w[1]);
     }
-    // role 0: dV^T[d][key] += dO^T P; role 1: dK^T[d][key] += Q^T dS
-    const char *src = role ? ql : dl;
+    const char *ql = (const char *)sm.q[sp];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int bt = 0; bt < 2; ++bt) {
-        const uint32_t o = cb + 16 * bt * RB;
-        acc[db] = mfma32x32x16(tr_operand_at(src, o, o + 8 * RB), fr[bt], acc[db]);
+        const uint32_t o = 16 * bt * RB;
+        acc[db] = mfma32x32x16(tr_operand_at(ql, o + so.trk[db][0], o + so.trk[db][1]),
+                               fr[bt], acc[db]);
       }
-    }
   };
 
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+    if (t < iters) issue(t);
+
   for (int it = 0; it < iters; ++it) {
-    const int buf = it % kDkvStages, nb = (it + kDkvStages - 1) % kDkvStages;
+    const int st = it % kDkvStages;
     const int r0 = rstart + (it % nrt) * kBR;
     // tile it has landed once at most the next tile's transfers are pending
     if (it + 1 < iters) wait_vmcnt_dyn(my_ops); else wait_vmcnt<0>();
-    // Tile it visible to all waves, and every wave is done reading tile
-    // it - 1 (its reads were consumed by MFMAs). A bare s_barrier: the fences
+    // Tile it visible to all waves; every wave is done with tile it - 2 and
+    // with the P buffer the P waves write next. A bare s_barrier: the fences
     // of __syncthreads() would also drain the transfers still in flight.
     lds_barrier();
-    const int tn = it + kDkvStages - 1;
-    const TileSrc ts = tile_src(tn < iters ? tn : it);
-    step(sm.q[buf], sm.dout[buf], sm.lse2[buf], sm.delta[buf], sm.lim[buf], sm.q[nb],
-         sm.dout[nb], sm.lse2[nb], sm.delta[nb], sm.lim[nb], ts.q, ts.d, ts.l, ts.dl, a.lim,
-         ts.r0, tn < iters, r0);
+    if (it + 2 < iters) issue(it + 2);
+    const int nvalid = min(kBR, e - r0);
+    const bool vis = wactive && sm.lim[st][nvalid - 1] >= kw0;
+    const char *ql = (const char *)sm.q[st];
+    const char *dl = (const char *)sm.dout[st];
+    if (pwave) {
+      if (!vis) continue;
+      // S[row][key] (rows 8i + 4hf + j of the accumulator)
+      f32x16 sacc;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        sacc = mfma32x32x16(*(const bf16x8 *)(ql + so.rowk[ks]), bop[ks],
+                            ks == 0 ? f32x16{} : sacc);
+      // rows at or past nvalid repeat the last row (clamped transfers) and
+      // are masked like keys past a row's bound
+      const bool full = nvalid == kBR && sm.lim[st][0] >= kw0 + 31;
+      const int key = kw0 + l32;
+      float *pp = sm.p[it & 1][pair];
+      bf16x8 fr[2] = {};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 l2 = *(const f32x4 *)&sm.lse2[st][8 * i + 4 * hf];
+        f32x4 pv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pv[j] = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
+        if (!full) {
+          const u32x4 li = *(const u32x4 *)&sm.lim[st][8 * i + 4 * hf];
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (8 * i + 4 * hf + j >= nvalid || key > (int)li[j]) pv[j] = 0.f;
+        }
+        *(f32x4 *)(pp + (i * 64 + lane) * 4) = pv;
+        put_rows(fr, i, f32x2{pv[0], pv[1]}, f32x2{pv[2], pv[3]});
+      }
+      // dV^T[d][key] += dO^T[d][row] P[row][key]
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int bt = 0; bt < 2; ++bt) {
+          const uint32_t o = 16 * bt * RB;
+          acc[db] = mfma32x32x16(tr_operand_at(dl, o + so.trk[db][0], o + so.trk[db][1]),
+                                 fr[bt], acc[db]);
+        }
+    } else {
+      if (vis_prev) ds_step((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1);
+      vis_prev = vis;
+      if (vis) {
+        // dP[row][key] = dO V^T for this tile, consumed in the next step
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+          dp = mfma32x32x16(*(const bf16x8 *)(dl + so.rowk[ks]), bop[ks],
+                            ks == 0 ? f32x16{} : dp);
+      }
+    }
   }
+  // the dS waves finish the last tile once its P is in LDS
+  lds_barrier();
+  if (!pwave && vis_prev) ds_step((iters - 1) % kDkvStages, (iters - 1) & 1);
 
   const int key = kw0 + l32;
   if (!wactive || key >= e) return;
-  float *out = (role ? a.dk : a.dv) + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
-  const float mul = role ? a.scale : 1.f;
+  float *out = (pwave ? a.dv : a.dk) + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
+  const float mul = pwave ? 1.f : a.scale;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -400,8 +394,8 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const int ntiles = (key_hi - s) / kBK + 1;
   DmaTile<D, kBK> dma;
   dma.init(tid, rs);
-  SwzOffsets so;
-  so.init(lane, RB);
+  SwzOffsets<D> so;
+  so.init(lane);
   const int64_t tile_elems = (int64_t)kBK * rs;
   const bf16_t *kt = kbase + (int64_t)s * rs;
   const bf16_t *vt = vbase + (int64_t)s * rs;
@@ -429,7 +423,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
         const char *vl = (const char *)sm.v[buf];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
-          const uint32_t o = kb * 32 * RB + 128 * (ks >> 2) + so.rowk[ks & 3];
+          const uint32_t o = kb * 32 * RB + so.rowk[ks];
           sacc = mfma32x32x16(*(const bf16x8 *)(kl + o), qf[ks], ks == 0 ? f32x16{} : sacc);
           pacc = mfma32x32x16(*(const bf16x8 *)(vl + o), df[ks], ks == 0 ? f32x16{} : pacc);
         }
@@ -454,11 +448,11 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
         }
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
 #pragma unroll
           for (int bt = 0; bt < 2; ++bt) {
-            const uint32_t o = cb + (kb * 32 + 16 * bt) * RB;
-            dq[db] = mfma32x32x16(tr_operand_at(kl, o, o + 8 * RB), dsf[bt], dq[db]);
+            const uint32_t o = (kb * 32 + 16 * bt) * RB;
+            dq[db] = mfma32x32x16(tr_operand_at(kl, o + so.trk[db][0], o + so.trk[db][1]),
+                                  dsf[bt], dq[db]);
           }
         }
       }

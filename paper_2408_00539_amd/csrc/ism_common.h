@@ -34,14 +34,20 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __shfl_xor(x, 32);
 }
 
+// IEEE 754-2019 maximum (NaN-propagating): one v_maximum3_f32 for up to three
+// operands, with none of the operand quieting that fmaxf needs.
+__device__ __forceinline__ float vmax(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);
+}
+
 // max / sum of x over lanes l and l ^ 32, via v_permlane32_swap: after the
 // swap of (x, x) the two results hold, in every lane, the lower-half and the
 // upper-half value of that lane pair.
 __device__ __forceinline__ float pair_max(float x) {
   const uint32_t u = __builtin_bit_cast(uint32_t, x);
   const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]),
-               __builtin_bit_cast(float, (uint32_t)r[1]));
+  return vmax(__builtin_bit_cast(float, (uint32_t)r[0]),
+              __builtin_bit_cast(float, (uint32_t)r[1]));
 }
 __device__ __forceinline__ float pair_sum(float x) {
   const uint32_t u = __builtin_bit_cast(uint32_t, x);
@@ -85,11 +91,18 @@ __device__ __forceinline__ bf16x8 tr_operand(const bf16_t *tile, int str, int m0
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Row swizzle of 16-byte chunks in unpadded LDS tiles: logical chunk c of
-// tile row r is stored at chunk c ^ swz(r). With 128- or 256-byte rows this
-// is conflict-free both for ds_read_b128 of 8 consecutive rows at one chunk
-// and for the 4 consecutive rows x 32 bytes of a ds_read_b64_tr_b16 group.
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+// Row swizzle of 16-byte chunks in unpadded LDS tiles of D bf16 per row:
+// logical chunk c of tile row r is stored at chunk c ^ swz<D>(r). It depends
+// on r % 16 only and takes 16 (D = 128) or 8 (D = 64) distinct values there,
+// so that both a ds_read_b128 of 16 consecutive rows at one chunk and the
+// 4 rows x 32 bytes of each ds_read_b64_tr_b16 lane group hit distinct banks
+// (64 banks of 4 bytes, 256 bytes per LDS cycle).
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  static_assert(D == 64 || D == 128, "head dim 64 or 128");
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return ((r >> 1) & 3) | ((((r >> 1) ^ (r >> 3)) & 1) << 2);
+}
 
 // Byte address of a pointer into LDS.
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
@@ -156,7 +169,7 @@ struct DmaTile {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = (i * NW + wave) * RPI + lane / CPR;
-      loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz(r)) * 8);
+      loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz<D>(r)) * 8);
     }
   }
 
@@ -178,7 +191,7 @@ struct DmaTile {
         if (q >= T) continue;
         const int r = q * RPI + lane / CPR;
         const int rr = min(r, nvalid - 1);
-        dma_x4(src + (int64_t)rr * rs + ((lane % CPR) ^ swz(r)) * 8, lb + q * 1024);
+        dma_x4(src + (int64_t)rr * rs + ((lane % CPR) ^ swz<D>(r)) * 8, lb + q * 1024);
       }
     }
   }
@@ -196,28 +209,32 @@ __device__ __forceinline__ bf16x8 tr_operand_at(const char *lds, uint32_t off_lo
 }
 
 // Per-lane byte offsets for reading MFMA A operands from a swizzled,
-// unpadded tile with RB-byte rows.
-//  * row operand (ds_read_b128): row r0 + (lane % 32) with r0 % 8 == 0, head
-//    chunks 2ks + h: offset = row(r0) + 128 (ks / 4) + rowk[ks % 4];
-//  * transposed operand (tr reads): rows k0 + 4h + lane_row, k0 % 16 == 0,
-//    columns 32 db + ...: offset = (db odd ? tro : tre) + 64 db + row(k0),
-//    and + 8 rows for the second read.
+// unpadded tile of D bf16 per row.
+//  * row operand (ds_read_b128): tile rows r0 + (lane % 32), r0 % 16 == 0,
+//    k step ks (head chunk 2 ks + lane / 32): byte row(r0) + rowk[ks];
+//  * transposed operand (two ds_read_b64_tr_b16, see tr_operand): tile rows
+//    k0 + ..., k0 % 16 == 0, head columns 32 db + ...: bytes row(k0) +
+//    trk[db][0] and row(k0) + trk[db][1] (the second read is 8 rows down).
+template <int D>
 struct SwzOffsets {
-  uint32_t rowk[4];
-  uint32_t tre, tro;
+  static constexpr int RB = D * 2;  // bytes per tile row
+  uint32_t rowk[D / 16];
+  uint32_t trk[D / 32][2];
 
-  __device__ __forceinline__ void init(int lane, int rb) {
+  __device__ __forceinline__ void init(int lane) {
     const int l32 = lane & 31, h = lane >> 5;
-    const int f = swz(l32);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) rowk[b] = (uint32_t)(l32 * rb + (((2 * b + h) ^ f) << 4));
-    const int g = lane >> 4, L = lane & 15, gh = g >> 1;
-    const int fv = ((L >> 2) << 1) | gh;
-    const int y = (2 * (g & 1) + ((L & 3) >> 1)) ^ fv;
-    const int yo = y - 8 * ((y >> 2) & 1);
-    const int base = (4 * gh + (L >> 2)) * rb + 8 * (L & 1);
-    tre = (uint32_t)(base + 16 * y);
-    tro = (uint32_t)(base + 16 * yo);
+    for (int ks = 0; ks < D / 16; ++ks)
+      rowk[ks] = (uint32_t)(l32 * RB + (((2 * ks + h) ^ swz<D>(l32)) << 4));
+    const int g = lane >> 4, L = lane & 15;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int r = 4 * (g >> 1) + (L >> 2) + 8 * s;
+        const int m = 32 * db + 16 * (g & 1) + 4 * (L & 3);
+        trk[db][s] = (uint32_t)(r * RB + (((m >> 3) ^ swz<D>(r)) << 4) + (m & 7) * 2);
+      }
   }
 };
 

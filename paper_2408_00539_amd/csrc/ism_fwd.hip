@@ -7,7 +7,7 @@
 // and a set of query heads that share one KV head: with G = hq / hkv query
 // heads per KV head, hpw = gcd(G, 4) heads run side by side (one per wave
 // column) so that the K/V tile staged in LDS serves all of them, and the
-// remaining 4 / hpw waves take consecutive 32*NQB-row blocks. Each wave
+// remaining 4 / hpw waves take consecutive 32-row blocks. Each wave
 // computes S^T = K Q^T for a 64-key tile (lane <-> query row, so the softmax
 // statistics of a row live in one lane pair), then O^T += V^T P^T.
 //
@@ -46,11 +46,7 @@ hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
   return hipGetLastError();
 }
 
-// Build-time tile configuration: rows per wave = 32 * ISM_FWD_NQB, and the
-// occupancy target in waves per SIMD (1 or 2) that bounds registers.
-#ifndef ISM_FWD_NQB
-#define ISM_FWD_NQB 1
-#endif
+// Occupancy target in waves per SIMD (1 or 2), which bounds registers.
 #ifndef ISM_FWD_WPE
 #define ISM_FWD_WPE 2
 #endif
@@ -58,9 +54,10 @@ hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
 namespace {
 
 constexpr int kBN = 64;  // keys per tile
+constexpr int kQW = 32;  // query rows per wave
 
 // K and V tiles of 64 keys, row-major, unpadded rows of D bf16 with the
-// swz() chunk swizzle, double-buffered; filled by direct global->LDS
+// swz<D>() chunk swizzle, double-buffered; filled by direct global->LDS
 // transfers. K is read as MFMA rows (ds_read_b128), V through transposing
 // reads (ds_read_b64_tr_b16) as the V^T operand.
 template <int D>
@@ -69,80 +66,177 @@ struct FwdSmem {
   bf16_t v[2][kBN * D];
 };
 
-// Online softmax of one 64-key tile held as S^T accumulators (lane <->
-// query row; the other 32 keys of the row sit in lane l ^ 32). Writes the
-// bf16 probabilities as B operands of the P V product.
-template <bool MASK, int NQB, int NDB>
-__device__ __forceinline__ void softmax_tile(f32x16 (&sacc)[2][NQB], int c0, int hf,
-                                             const int (&lim_r)[NQB], float sl2, float tau,
-                                             float (&m_run)[NQB], float (&l_run)[NQB],
-                                             f32x16 (&oacc)[NDB][NQB],
-                                             bf16x8 (&pf)[NQB][2][2]) {
-  float mt[NQB];
-  bool grow = false;
+// S^T[key][row] = K Q^T for one 64-key tile: two 32-key blocks, D/16 steps.
+template <int D>
+__device__ __forceinline__ void tile_scores(const char *kl, const SwzOffsets<D> &so,
+                                            const bf16x8 (&qf)[D / 16], f32x16 (&s)[2]) {
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    float x = -INFINITY;
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (MASK) {
-          const int key = c0 + kb * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-          if (key > lim_r[qb]) sacc[kb][qb][r] = -INFINITY;
-        }
-        x = fmaxf(x, sacc[kb][qb][r]);
-      }
-    mt[qb] = pair_max(x);
-    grow |= mt[qb] > m_run[qb] + tau;
-  }
-  if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      const float mnew = fmaxf(m_run[qb], mt[qb]);
-      const float alpha = fast_exp2((m_run[qb] - mnew) * sl2);
-      m_run[qb] = mnew;
-      l_run[qb] *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[db][qb][r] *= alpha;
+    for (int ks = 0; ks < D / 16; ++ks) {
+      const bf16x8 kf = *(const bf16x8 *)(kl + kb * 32 * D * 2 + so.rowk[ks]);
+      s[kb] = mfma32x32x16(kf, qf[ks], ks == 0 ? f32x16{} : s[kb]);
     }
-  }
+}
+
+// Keys past the row's bound lim get score -inf.
+__device__ __forceinline__ void tile_mask(f32x16 (&s)[2], int c0, int hf, int lim) {
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    const float moff = m_run[qb] * sl2;
-    float rsum = 0.f;
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = c0 + kb * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
+      if (key > lim) s[kb][r] = -INFINITY;
+    }
+}
+
+// Row max of a tile, combined over the lane pair that holds the row.
+__device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
+  float x[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) x[r & 3] = vmax(x[r & 3], vmax(s[kb][r], s[kb][r + 1]));
+  return pair_max(vmax(vmax(x[0], x[2]), vmax(x[1], x[3])));
+}
+
+// Lazy online-softmax update: the reference max is only raised when a row's
+// tile max exceeds it by more than tau (2^8 in probability units); exact
+// either way since numerator and denominator share the reference max.
+template <int NDB>
+__device__ __forceinline__ void raise_max(float mt, float sl2, float tau, float &m_run,
+                                          float &l_run, f32x16 (&oacc)[NDB]) {
+  if (__builtin_amdgcn_ballot_w64(mt > m_run + tau) != 0) {
+    const float mnew = vmax(m_run, mt);
+    const float alpha = fast_exp2((m_run - mnew) * sl2);
+    m_run = mnew;
+    l_run *= alpha;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+  }
+}
+
+// Probabilities 2^(s sl2 - moff) of one tile as bf16 B operands of the P V
+// product, and their fp32 row sum.
+__device__ __forceinline__ float tile_probs(const f32x16 (&s)[2], float sl2, float moff,
+                                            bf16x8 (&pf)[2][2]) {
+  float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int bt = 0; bt < 2; ++bt) {
+      u32x4 w;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        f32x2 p;
+        p[0] = fast_exp2(fmaf(s[kb][8 * bt + 2 * u], sl2, -moff));
+        p[1] = fast_exp2(fmaf(s[kb][8 * bt + 2 * u + 1], sl2, -moff));
+        sum[u] += p[0] + p[1];
+        w[u] = cvt_bf16x2(p);
+      }
+      pf[kb][bt] = __builtin_bit_cast(bf16x8, w);
+    }
+  return (sum[0] + sum[1]) + (sum[2] + sum[3]);
+}
+
+// O^T[d][row] += V^T[d][key] P^T[key][row] for one 64-key tile.
+template <int D>
+__device__ __forceinline__ void tile_pv(const char *vl, const SwzOffsets<D> &so,
+                                        const bf16x8 (&pf)[2][2], f32x16 (&oacc)[D / 32]) {
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int bt = 0; bt < 2; ++bt) {
-        f32x2 p[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          p[u][0] = fast_exp2(fmaf(sacc[kb][qb][8 * bt + 2 * u], sl2, -moff));
-          p[u][1] = fast_exp2(fmaf(sacc[kb][qb][8 * bt + 2 * u + 1], sl2, -moff));
-          rsum += p[u][0] + p[u][1];
-        }
-        u32x4 w;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) w[u] = cvt_bf16x2(p[u]);
-        pf[qb][kb][bt] = __builtin_bit_cast(bf16x8, w);
+        const uint32_t o = (kb * 32 + 16 * bt) * D * 2;
+        const bf16x8 vf = tr_operand_at(vl, o + so.trk[db][0], o + so.trk[db][1]);
+        oacc[db] = mfma32x32x16(vf, pf[kb][bt], oacc[db]);
       }
-    l_run[qb] += rsum;
   }
 }
 
-template <int D, int NQB, bool CACHE>
+// One pipelined step in a fixed instruction order: the D/8 products of
+// S(t+1) = K(t+1) Q^T, then the D/8 products of O^T += V(t)^T P(t)^T (64-key
+// chunks outermost, so consecutive products use different accumulators).
+// Each product is followed by the LDS read of the operand LA products ahead
+// (K rows, then transposed V) and by its share of the vector work: during
+// the S products the exponentials, row sums and bf16 packing of tile t,
+// during the P V products the row max of S(t+1). The order is pinned with
+// scheduling barriers so that the matrix core and the vector ALU of a wave
+// are busy at the same time. Returns the fp32 row sum of P(t); mt receives
+// the (unmasked) row max of S(t+1).
+template <int D>
+__device__ __forceinline__ float step_block(const char *kl, const char *vl,
+                                            const SwzOffsets<D> &so, const bf16x8 (&qf)[D / 16],
+                                            const f32x16 (&cur)[2], f32x16 (&nxt)[2],
+                                            f32x16 (&oacc)[D / 32], float sl2, float moff,
+                                            float &mt) {
+  constexpr int NKS = D / 16, NDB = D / 32;
+  constexpr int NS = 2 * NKS, NP = 4 * NDB, N = NS + NP, LA = 3;
+  constexpr int PPS = 16 / NS;  // probability pairs per S product
+  constexpr int MPP = 32 / NP;  // max elements per P V product
+  auto read = [&](int n) -> bf16x8 {
+    if (n < NS) {
+      const int kb = n / NKS, ks = n % NKS;
+      return *(const bf16x8 *)(kl + kb * 32 * D * 2 + so.rowk[ks]);
+    }
+    const int j = n - NS, kc = j / NDB, db = j % NDB;
+    const uint32_t o = ((kc >> 1) * 32 + 16 * (kc & 1)) * D * 2;
+    return tr_operand_at(vl, o + so.trk[db][0], o + so.trk[db][1]);
+  };
+  bf16x8 op[N];
+#pragma unroll
+  for (int n = 0; n < LA; ++n) op[n] = read(n);
+  u32x4 w[2][2];
+  float sum[2] = {0.f, 0.f}, mx[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    if (n < NS) {
+      const int kb = n / NKS, ks = n % NKS;
+      nxt[kb] = mfma32x32x16(op[n], qf[ks], ks == 0 ? f32x16{} : nxt[kb]);
+    } else {
+      const int j = n - NS, kc = j / NDB, db = j % NDB;
+      oacc[db] = mfma32x32x16(op[n], __builtin_bit_cast(bf16x8, w[kc >> 1][kc & 1]), oacc[db]);
+    }
+    if (n + LA < N) op[n + LA] = read(n + LA);
+    if (n < NS) {
+#pragma unroll
+      for (int c = 0; c < PPS; ++c) {
+        const int i = n * PPS + c, kb = i >> 3, bt = (i >> 2) & 1, u = i & 3;
+        f32x2 p;
+        p[0] = fast_exp2(fmaf(cur[kb][8 * bt + 2 * u], sl2, -moff));
+        p[1] = fast_exp2(fmaf(cur[kb][8 * bt + 2 * u + 1], sl2, -moff));
+        sum[i & 1] += p[0] + p[1];
+        w[kb][bt][u] = cvt_bf16x2(p);
+        asm volatile("" : "+v"(sum[i & 1]));  // keep the add in this slot
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < MPP; c += 2) {
+        const int e = (n - NS) * MPP + c, m = (e >> 1) & 1;
+        mx[m] = vmax(mx[m], vmax(nxt[e >> 4][e & 15], nxt[e >> 4][(e & 15) + 1]));
+        asm volatile("" : "+v"(mx[m]));
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  mt = pair_max(vmax(mx[0], mx[1]));
+  return sum[0] + sum[1];
+}
+
+template <int D, bool CACHE>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
 fwd_kernel(FwdArgs a, int hpw, int tiles) {
-  constexpr int QW = NQB * 32;     // rows per wave
   constexpr int NDB = D / 32;      // 32-wide d blocks of the output
   constexpr int NKS = D / 16;      // 16-deep k steps of Q K^T
   __shared__ FwdSmem<D> sm;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int l32 = lane & 31, hf = lane >> 5;
 
   // Work item: XCD-aware (consecutive workgroups land on different XCDs, so
@@ -157,14 +251,14 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
   const int tile = tiles - 1 - item % tiles;
   const int b = group / hsets;
   const int head0 = (group % hsets) * hpw;
-  const int wg_rows = (4 / hpw) * QW;
+  const int wg_rows = (4 / hpw) * kQW;
   const int s = a.cu_q[b], e = a.cu_q[b + 1];
   const int q0 = s + tile * wg_rows;
   if (q0 >= e) return;
 
   const int head = head0 + wave % hpw;
   const int kvh = head0 / (a.hq / a.hkv);
-  const int wq0 = q0 + (wave / hpw) * QW;
+  const int wq0 = q0 + (wave / hpw) * kQW;
   const bool active = wq0 < e;
   const int wg_last = min(q0 + wg_rows, e) - 1;
 
@@ -183,131 +277,110 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
     key_begin = s;
     key_hi = a.lim[wg_last];
     wave_lo = a.lim[min(wq0, e - 1)];
-    wave_hi = active ? a.lim[min(wq0 + QW, e) - 1] : s - 1;
+    wave_hi = active ? a.lim[min(wq0 + kQW, e) - 1] : s - 1;
     kbase = (const bf16_t *)a.k + (int64_t)kvh * a.kv_head_stride;
     vbase = (const bf16_t *)a.v + (int64_t)kvh * a.kv_head_stride;
   }
   const int64_t rs = a.kv_row_stride;
   const float sl2 = a.scale * kLog2e;
+  // lazy rescale threshold: 2^8 in probability units
+  const float tau = 8.f / sl2;
 
-  // Per-lane query rows (clamped into the dialogue; rows past e are computed
+  // Per-lane query row (clamped into the dialogue; rows past e are computed
   // as copies of the last row and never stored).
-  int lim_r[NQB];
-  bf16x8 qf[NQB][NKS];
-#pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    const int rc = min(wq0 + qb * 32 + l32, e - 1);
-    lim_r[qb] = CACHE ? key_hi : a.lim[rc];
+  const int rc = min(wq0 + l32, e - 1);
+  const int lim_r = CACHE ? key_hi : a.lim[rc];
+  bf16x8 qf[NKS];
+  {
     const bf16_t *qp = (const bf16_t *)a.q + ((int64_t)rc * a.hq + head) * D + hf * 8;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qf[qb][ks] = *(const bf16x8 *)(qp + ks * 16);
+    for (int ks = 0; ks < NKS; ++ks) qf[ks] = *(const bf16x8 *)(qp + ks * 16);
   }
   wait_loads();
 
-  f32x16 oacc[NDB][NQB];
+  f32x16 oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[db][qb][r] = 0.f;
-  float m_run[NQB], l_run[NQB];
-#pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.f; }
+    for (int r = 0; r < 16; ++r) oacc[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
 
-  // lazy rescaling: the running max is only raised when a row's tile max
-  // exceeds it by more than 2^8 in probability units (exact either way:
-  // numerator and denominator share the reference max)
-  const float tau = 8.f / sl2;
-  bf16x8 pf[NQB][2][2];
-
-  const int ntiles = (key_hi - key_begin) / kBN + 1;
+  // Software pipeline over key tiles. Tile t's scores S(t) are complete (and
+  // masked, the running max raised) when step t starts; step t then issues
+  // S(t+1) = K(t+1) Q^T and the P(t) V(t) product in the same basic block as
+  // the exponentials of tile t, so matrix and vector work of one wave
+  // overlap. LDS holds K(t+1) and V(t) during step t while K(t+2) and V(t+1)
+  // are in flight into the other halves of the double buffers.
+  const int ntiles = (key_hi - key_begin) / kBN + 1;  // for the workgroup
+  const int nw = active ? (wave_hi - key_begin) / kBN + 1 : 0;  // this wave's
   DmaTile<D, kBN> dma;
   dma.init(tid, rs);
-  SwzOffsets so;
-  so.init(lane, D * 2);
+  SwzOffsets<D> so;
+  so.init(lane);
   const int64_t tile_elems = (int64_t)kBN * rs;
   const bf16_t *kt = kbase + (int64_t)key_begin * rs;
   const bf16_t *vt = vbase + (int64_t)key_begin * rs;
   dma.issue(kt, rs, key_hi - key_begin + 1, sm.k[0]);
   dma.issue(vt, rs, key_hi - key_begin + 1, sm.v[0]);
+  if (ntiles > 1) dma.issue(kt + tile_elems, rs, key_hi - key_begin - kBN + 1, sm.k[1]);
   wait_vmem();
   __syncthreads();
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
+  f32x16 sa[2], sb[2];
+  if (nw > 0) {
+    tile_scores<D>((const char *)sm.k[0], so, qf, sa);
+    if (key_begin + kBN - 1 > wave_lo) tile_mask(sa, key_begin, hf, lim_r);
+    raise_max(tile_max(sa), sl2, tau, m_run, l_run, oacc);
+  }
+  lds_barrier();  // every wave is done with K(0) before K(2) overwrites it
+
+  auto step = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], int t) {
     const int c0 = key_begin + t * kBN;
-    if (t + 1 < ntiles) {
-      kt += tile_elems;
-      vt += tile_elems;
-      dma.issue(kt, rs, key_hi - (c0 + kBN) + 1, sm.k[buf ^ 1]);
-      dma.issue(vt, rs, key_hi - (c0 + kBN) + 1, sm.v[buf ^ 1]);
-    }
-
-    if (active && c0 <= wave_hi) {
-      // S^T[key][row] for two 32-key blocks
-      f32x16 sacc[2][NQB];
-      const char *kl = (const char *)sm.k[buf];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const bf16x8 kf = *(const bf16x8 *)(kl + kb * 32 * D * 2 + 128 * (ks >> 2) +
-                                              so.rowk[ks & 3]);
-#pragma unroll
-          for (int qb = 0; qb < NQB; ++qb)
-            sacc[kb][qb] = mfma32x32x16(kf, qf[qb][ks], ks == 0 ? f32x16{} : sacc[kb][qb]);
+    if (t + 2 < ntiles)
+      dma.issue(kt + 2 * tile_elems, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
+    if (t + 1 < ntiles)
+      dma.issue(vt + tile_elems, rs, key_hi - (c0 + kBN) + 1, sm.v[(t + 1) & 1]);
+    kt += tile_elems;
+    vt += tile_elems;
+    const char *kl = (const char *)sm.k[(t + 1) & 1];
+    const char *vl = (const char *)sm.v[t & 1];
+    if (t < nw) {
+      // the last tile of a wave also computes an (unused) S(t+1) from
+      // whatever the K buffer holds, which keeps one code path per step
+      float mt;
+      l_run += step_block<D>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt);
+      if (t + 1 < nw) {
+        if (c0 + 2 * kBN - 1 > wave_lo) {  // S(t+1) crosses some row's bound
+          tile_mask(nxt, c0 + kBN, hf, lim_r);
+          mt = tile_max(nxt);
         }
-      }
-      // only tiles that cross some row's bound pay for the mask
-      if (c0 + kBN - 1 <= wave_lo) {
-        softmax_tile<false>(sacc, c0, hf, lim_r, sl2, tau, m_run, l_run, oacc, pf);
-      } else {
-        softmax_tile<true>(sacc, c0, hf, lim_r, sl2, tau, m_run, l_run, oacc, pf);
-      }
-
-      // O^T[d][row] += V^T[d][key] P^T[key][row]
-      const char *vl = (const char *)sm.v[buf];
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const uint32_t cb = ((db & 1) ? so.tro : so.tre) + 64 * db;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int bt = 0; bt < 2; ++bt) {
-            const uint32_t o = cb + (kb * 32 + 16 * bt) * D * 2;
-            const bf16x8 vf = tr_operand_at(vl, o, o + 8 * D * 2);
-#pragma unroll
-            for (int qb = 0; qb < NQB; ++qb)
-              oacc[db][qb] = mfma32x32x16(vf, pf[qb][kb][bt], oacc[db][qb]);
-          }
+        raise_max(mt, sl2, tau, m_run, l_run, oacc);
       }
     }
-
     wait_vmem();
     __syncthreads();
+  };
+  for (int t = 0; t < ntiles; t += 2) {
+    step(sa, sb, t);
+    if (t + 1 < ntiles) step(sb, sa, t + 1);
   }
 
   if (!active) return;
+  const float lt = pair_sum(l_run);
+  const int row = wq0 + l32;
+  if (row >= e) return;
+  const float inv = 1.f / lt;
+  bf16_t *op = (bf16_t *)a.o + ((int64_t)row * a.hq + head) * D + hf * 4;
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) {
-    const float lt = pair_sum(l_run[qb]);
-    const int row = wq0 + qb * 32 + l32;
-    if (row >= e) continue;
-    const float inv = 1.f / lt;
-    bf16_t *op = (bf16_t *)a.o + ((int64_t)row * a.hq + head) * D + hf * 4;
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u32x2 w;
-        w[0] = pack_bf16x2(oacc[db][qb][4 * i + 0] * inv, oacc[db][qb][4 * i + 1] * inv);
-        w[1] = pack_bf16x2(oacc[db][qb][4 * i + 2] * inv, oacc[db][qb][4 * i + 3] * inv);
-        *(u32x2 *)(op + db * 32 + 8 * i) = w;
-      }
-    if (a.lse && hf == 0)
-      a.lse[(int64_t)head * a.total_q + row] = m_run[qb] * a.scale + logf(lt);
-  }
+    for (int i = 0; i < 4; ++i) {
+      u32x2 w;
+      w[0] = pack_bf16x2(oacc[db][4 * i + 0] * inv, oacc[db][4 * i + 1] * inv);
+      w[1] = pack_bf16x2(oacc[db][4 * i + 2] * inv, oacc[db][4 * i + 3] * inv);
+      *(u32x2 *)(op + db * 32 + 8 * i) = w;
+    }
+  if (a.lse && hf == 0) a.lse[(int64_t)head * a.total_q + row] = m_run * a.scale + logf(lt);
 }
 
 int gcd_int(int x, int y) {
@@ -317,14 +390,13 @@ int gcd_int(int x, int y) {
 
 template <int D, bool CACHE>
 hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
-  constexpr int NQB = ISM_FWD_NQB;
   const int hpw = gcd_int(a.hq / a.hkv, 4);
-  const int wg_rows = (4 / hpw) * NQB * 32;
+  const int wg_rows = (4 / hpw) * kQW;
   const int tiles = (a.max_rows + wg_rows - 1) / wg_rows;
   const int64_t total = (int64_t)a.batch * (a.hq / hpw) * tiles;
   if (total == 0) return hipSuccess;
   const int64_t per = (total + 7) / 8;
-  hipLaunchKernelGGL((fwd_kernel<D, NQB, CACHE>), dim3((unsigned)(8 * per)),
+  hipLaunchKernelGGL((fwd_kernel<D, CACHE>), dim3((unsigned)(8 * per)),
                      dim3(256), 0, stream, a, hpw, tiles);
   return hipGetLastError();
 }
