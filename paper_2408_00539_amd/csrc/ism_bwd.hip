@@ -17,6 +17,8 @@
 //     S^T and dP^T per 64-key tile and accumulates dQ^T += K^T dS^T.
 // All products are bf16 MFMA 32x32x16 with fp32 accumulation; gradients are
 // written in fp32.
+#include <type_traits>
+
 #include "ism_common.h"
 #include "ism_kernels.h"
 
@@ -87,7 +89,7 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 constexpr int kDkvStages = 4;
 
 // Q and dO tiles of 32 rows (unpadded swizzled rows, see swz<D>()) plus the
-// per-row LSE (log2 units), delta and lim, all filled by direct global->LDS
+// per-row LSE (log2 units) and delta, all filled by direct global->LDS
 // transfers; and P of the last two tiles for each wave pair, fp32 in MFMA
 // accumulator layout (lane-private, 16 values per lane, stored as 4 x 16
 // bytes so that consecutive lanes touch consecutive bytes).
@@ -97,7 +99,6 @@ struct DkvSmem {
   bf16_t dout[kDkvStages][kBR * D];
   __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
   __attribute__((aligned(16))) float delta[kDkvStages][kBR];
-  __attribute__((aligned(16))) int lim[kDkvStages][kBR];
   __attribute__((aligned(16))) float p[2][4][16 * 64];
 };
 
@@ -129,7 +130,7 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
 }
 
 // fr[bt] slots of the B operand (16 rows x 32 keys) from four accumulator
-// rows groups: accumulator rows 8i..8i+3 (+4 for the upper half-wave) are
+// row groups: accumulator rows 8i..8i+3 (+4 for the upper half-wave) are
 // slots 4 (i & 1) .. of operand i >> 1, matching the k order of the
 // transposing A-operand reads.
 __device__ __forceinline__ void put_rows(bf16x8 (&fr)[2], int i, f32x2 lo, f32x2 hi) {
@@ -140,20 +141,42 @@ __device__ __forceinline__ void put_rows(bf16x8 (&fr)[2], int i, f32x2 lo, f32x2
   fr[bt] = __builtin_bit_cast(bf16x8, x);
 }
 
+// N products in a fixed order: product n consumes operand n, read from LDS
+// LA products ahead; mid() (vector work that later products depend on)
+// runs before product K. Scheduling barriers pin the order.
+template <int N, int K, int LA, class Rd, class Mm, class Mid>
+__device__ __forceinline__ void product_stream(Rd &&rd, Mm &&mm, Mid &&mid) {
+  bf16x8 op[N];
+#pragma unroll
+  for (int n = 0; n < LA && n < N; ++n) op[n] = rd(n);
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    if (n == K) {
+      mid();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    mm(n, op[n]);
+    if (n + LA < N) op[n + LA] = rd(n + LA);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Eight waves in four pairs; pair p owns the 32 keys c0 + 32 p (lane <->
 // key) and its two waves share one SIMD:
 //  * the P wave (p) computes S = Q K^T and P = exp(S - LSE) (masked) for
 //    tile t, accumulates dV^T += dO^T P and leaves P in LDS;
-//  * the dS wave (p + 4) computes dP = dO V^T for tile t and, one tile
-//    behind, dS = P o (dP - delta) with its partner's P, dK^T += Q^T dS.
+//  * the dS wave (p + 4), one tile behind, forms dS = P o (dP - delta) with
+//    its partner's P and accumulates dK^T += Q^T dS, then computes
+//    dP = dO V^T of tile t for the next step.
 // Each wave does 16 of the 32 products per tile with no product computed
 // twice, and the exp / elementwise phase of one wave of a pair falls in the
-// other's MFMA phase.
+// other's MFMA phase. Visibility needs no per-row bounds: row r sees key i
+// exactly when r >= seer[i] (seer is non-decreasing in i).
 template <int D>
 __global__ void __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(ISM_DKV_WPE, ISM_DKV_WPE)))
 dkv_kernel(BwdArgs a, int ktiles) {
-  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2;
+  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2, LA = 3;
   __shared__ DkvSmem<D> sm;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -177,13 +200,19 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int G = a.hq / a.hkv;
   const float sl2 = a.scale * kLog2e;
 
+  // first rows that see the wave's first and last key, and this lane's key
+  const int seer_first = wactive ? a.seer[kw0] : e;
+  const int seer_last = (wactive && kw0 + 31 < e) ? a.seer[kw0 + 31] : e;
+  const int key = kw0 + l32;
+  const int seer_k = key < e ? a.seer[key] : 0x7fffffff;
+
   // B operands of this wave's products: K (P wave, for S) or V (dS wave,
   // for dP) of its 32 keys, lane <-> key, 8 head-dim values per k step
   bf16x8 bop[NKS];
   {
-    const int key = min(kw0 + l32, e - 1);
+    const int kr = min(key, e - 1);
     const bf16_t *src =
-        (const bf16_t *)(pwave ? a.k : a.v) + ((int64_t)key * a.hkv + kvh) * D + hf * 8;
+        (const bf16_t *)(pwave ? a.k : a.v) + ((int64_t)kr * a.hkv + kvh) * D + hf * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) bop[ks] = *(const bf16x8 *)(src + ks * 16);
     wait_loads();
@@ -191,7 +220,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
-  f32x16 dp = {};        // dS wave: dP of the previous tile
+  f32x16 dp = {};         // dS wave: dP of the previous tile
   bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   const int rstart = a.seer[c0];
@@ -203,117 +232,161 @@ dkv_kernel(BwdArgs a, int ktiles) {
   SwzOffsets<D> so;
   so.init(lane);
   // transfers this wave issues per tile: Q and dO blocks, plus one row-scalar
-  // array for waves 5, 6, 7
-  const int my_ops = 2 * (wave < DmaTile<D, kBR, 8>::T ? 1 : 0) + (wave >= 5 ? 1 : 0);
-  auto issue = [&](int t) {
-    const int st = t % kDkvStages;
-    const int h = kvh * G + t / nrt, r0 = rstart + (t % nrt) * kBR;
-    const int64_t base = ((int64_t)r0 * a.hq + h) * D;
+  // array for waves 6 and 7
+  const int my_ops = 2 * (wave < DmaTile<D, kBR, 8>::T ? 1 : 0) + (wave >= 6 ? 1 : 0);
+  // next tile to transfer: index, head, row tile
+  int nx = 0, nx_h = kvh * G, nx_rt = 0;
+  auto issue_next = [&]() {
+    const int st = nx % kDkvStages, r0 = rstart + nx_rt * kBR;
+    const int64_t base = ((int64_t)r0 * a.hq + nx_h) * D;
     dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[st]);
     dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[st]);
-    if (wave == 5) dma_row_scalars(a.lse2 + (int64_t)h * a.total, r0, e - 1, sm.lse2[st], lane);
-    if (wave == 6) dma_row_scalars(a.delta + (int64_t)h * a.total, r0, e - 1, sm.delta[st], lane);
-    if (wave == 7) dma_row_scalars(a.lim, r0, e - 1, sm.lim[st], lane);
+    if (wave == 6) dma_row_scalars(a.lse2 + (int64_t)nx_h * a.total, r0, e - 1, sm.lse2[st], lane);
+    if (wave == 7) dma_row_scalars(a.delta + (int64_t)nx_h * a.total, r0, e - 1, sm.delta[st], lane);
+    ++nx;
+    if (++nx_rt == nrt) { nx_rt = 0; ++nx_h; }
   };
 
-  // dS wave: dS = P o (dP - delta) for the tile in stage sp (P from pbuf),
-  // then dK^T[d][key] += Q^T[d][row] dS[row][key].
-  auto ds_step = [&](int sp, int pbuf) {
-    const float *pp = sm.p[pbuf][pair];
-    bf16x8 fr[2] = {};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const f32x4 pv = *(const f32x4 *)(pp + (i * 64 + lane) * 4);
-      const f32x4 dlt = *(const f32x4 *)&sm.delta[sp][8 * i + 4 * hf];
-      f32x2 w[2];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) w[j >> 1][j & 1] = pv[j] * (dp[4 * i + j] - dlt[j]);
-      put_rows(fr, i, w[0], w[1]);
-    }
+  // dS wave: dS = P o (dP - delta) for the previous tile (stage sp, P buffer
+  // pbuf), dK^T[d][key] += Q^T[d][row] dS[row][key]; then, if dl is set,
+  // dP[row][key] = dO V^T of the current tile.
+  auto ds_dp = [&](int sp, int pbuf, const char *dl, auto has_ds, auto has_dp) {
+    constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
+    constexpr int NK = DS ? 2 * NDB : 0, N = NK + (DP ? NKS : 0);
     const char *ql = (const char *)sm.q[sp];
+    const float *pp = sm.p[pbuf][pair];
+    f32x4 pv[4], dlt[4];
+    if (DS) {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int bt = 0; bt < 2; ++bt) {
-        const uint32_t o = 16 * bt * RB;
-        acc[db] = mfma32x32x16(tr_operand_at(ql, o + so.trk[db][0], o + so.trk[db][1]),
-                               fr[bt], acc[db]);
+      for (int i = 0; i < 4; ++i) {
+        pv[i] = *(const f32x4 *)(pp + (i * 64 + lane) * 4);
+        dlt[i] = *(const f32x4 *)&sm.delta[sp][8 * i + 4 * hf];
       }
+    }
+    bf16x8 fr[2] = {};
+    auto rd = [&](int n) -> bf16x8 {
+      if (n < NK) {
+        const uint32_t o = 16 * (n & 1) * RB;
+        return tr_operand_at(ql, o + so.trk[n >> 1][0], o + so.trk[n >> 1][1]);
+      }
+      return *(const bf16x8 *)(dl + so.rowk[n - NK]);
+    };
+    f32x16 dpn;
+    auto mm = [&](int n, bf16x8 x) {
+      if (n < NK) {
+        acc[n >> 1] = mfma32x32x16(x, fr[n & 1], acc[n >> 1]);
+      } else {
+        const int ks = n - NK;
+        dpn = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dpn);
+      }
+    };
+    auto mid = [&]() {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x2 w[2];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j >> 1][j & 1] = pv[i][j] * (dp[4 * i + j] - dlt[i][j]);
+        put_rows(fr, i, w[0], w[1]);
+      }
+    };
+    product_stream<N, DS ? 0 : -1, LA>(rd, mm, mid);
+    if (DP) dp = dpn;
   };
 
+  // P wave on the current tile (stage st, rows r0.., nvalid valid): S, P
+  // (masked unless every row sees every key) to LDS and into operand form,
+  // dV^T += dO^T P.
+  auto p_dv = [&](int st, int r0, int nvalid, int pbuf, bool full) {
+    const char *ql = (const char *)sm.q[st];
+    const char *dl = (const char *)sm.dout[st];
+    f32x4 l2[4];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
-    if (t < iters) issue(t);
+    for (int i = 0; i < 4; ++i) l2[i] = *(const f32x4 *)&sm.lse2[st][8 * i + 4 * hf];
+    float *pp = sm.p[pbuf][pair];
+    f32x16 sacc;
+    bf16x8 fr[2] = {};
+    auto rd = [&](int n) -> bf16x8 {
+      if (n < NKS) return *(const bf16x8 *)(ql + so.rowk[n]);
+      const int j = n - NKS;
+      const uint32_t o = 16 * (j & 1) * RB;
+      return tr_operand_at(dl, o + so.trk[j >> 1][0], o + so.trk[j >> 1][1]);
+    };
+    auto mm = [&](int n, bf16x8 x) {
+      if (n < NKS) {
+        sacc = mfma32x32x16(x, bop[n], n == 0 ? f32x16{} : sacc);
+      } else {
+        const int j = n - NKS;
+        acc[j >> 1] = mfma32x32x16(x, fr[j & 1], acc[j >> 1]);
+      }
+    };
+    auto mid = [&]() {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x4 pv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pv[j] = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[i][j]));
+        if (!full) {
+          // rows at or past nvalid repeat the last row (clamped transfers)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int rr = 8 * i + 4 * hf + j;
+            if (rr >= nvalid || r0 + rr < seer_k) pv[j] = 0.f;
+          }
+        }
+        *(f32x4 *)(pp + (i * 64 + lane) * 4) = pv;
+        put_rows(fr, i, f32x2{pv[0], pv[1]}, f32x2{pv[2], pv[3]});
+      }
+    };
+    product_stream<NKS + 2 * NDB, NKS, LA>(rd, mm, mid);
+  };
 
-  for (int it = 0; it < iters; ++it) {
-    const int st = it % kDkvStages;
-    const int r0 = rstart + (it % nrt) * kBR;
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  if (iters > 0) issue_next();
+  if (iters > 1) issue_next();
+  // Start of step it (row tile rt): wait for its tile, synchronize, start
+  // the transfer of a later tile. Returns the tile's first row.
+  auto begin_step = [&](int it, int &rt) {
+    const int r0 = rstart + rt * kBR;
+    if (++rt == nrt) rt = 0;
     // tile it has landed once at most the next tile's transfers are pending
     if (it + 1 < iters) wait_vmcnt_dyn(my_ops); else wait_vmcnt<0>();
     // Tile it visible to all waves; every wave is done with tile it - 2 and
     // with the P buffer the P waves write next. A bare s_barrier: the fences
     // of __syncthreads() would also drain the transfers still in flight.
     lds_barrier();
-    if (it + 2 < iters) issue(it + 2);
-    const int nvalid = min(kBR, e - r0);
-    const bool vis = wactive && sm.lim[st][nvalid - 1] >= kw0;
-    const char *ql = (const char *)sm.q[st];
-    const char *dl = (const char *)sm.dout[st];
-    if (pwave) {
-      if (!vis) continue;
-      // S[row][key] (rows 8i + 4hf + j of the accumulator)
-      f32x16 sacc;
-#pragma unroll
-      for (int ks = 0; ks < NKS; ++ks)
-        sacc = mfma32x32x16(*(const bf16x8 *)(ql + so.rowk[ks]), bop[ks],
-                            ks == 0 ? f32x16{} : sacc);
-      // rows at or past nvalid repeat the last row (clamped transfers) and
-      // are masked like keys past a row's bound
-      const bool full = nvalid == kBR && sm.lim[st][0] >= kw0 + 31;
-      const int key = kw0 + l32;
-      float *pp = sm.p[it & 1][pair];
-      bf16x8 fr[2] = {};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const f32x4 l2 = *(const f32x4 *)&sm.lse2[st][8 * i + 4 * hf];
-        f32x4 pv;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) pv[j] = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[j]));
-        if (!full) {
-          const u32x4 li = *(const u32x4 *)&sm.lim[st][8 * i + 4 * hf];
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (8 * i + 4 * hf + j >= nvalid || key > (int)li[j]) pv[j] = 0.f;
-        }
-        *(f32x4 *)(pp + (i * 64 + lane) * 4) = pv;
-        put_rows(fr, i, f32x2{pv[0], pv[1]}, f32x2{pv[2], pv[3]});
-      }
-      // dV^T[d][key] += dO^T[d][row] P[row][key]
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int bt = 0; bt < 2; ++bt) {
-          const uint32_t o = 16 * bt * RB;
-          acc[db] = mfma32x32x16(tr_operand_at(dl, o + so.trk[db][0], o + so.trk[db][1]),
-                                 fr[bt], acc[db]);
-        }
-    } else {
-      if (vis_prev) ds_step((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1);
-      vis_prev = vis;
-      if (vis) {
-        // dP[row][key] = dO V^T for this tile, consumed in the next step
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-          dp = mfma32x32x16(*(const bf16x8 *)(dl + so.rowk[ks]), bop[ks],
-                            ks == 0 ? f32x16{} : dp);
-      }
+    if (nx < iters) issue_next();
+    return r0;
+  };
+  // The two roles run separate loops (same barrier count) so that each
+  // keeps its accumulators in place.
+  int rt = 0;
+  if (pwave) {
+    for (int it = 0; it < iters; ++it) {
+      const int r0 = begin_step(it, rt);
+      const int nvalid = min(kBR, e - r0);
+      if (r0 + nvalid - 1 < seer_first) continue;  // no row sees these keys
+      p_dv(it % kDkvStages, r0, nvalid, it & 1, nvalid == kBR && r0 >= seer_last);
     }
+    lds_barrier();
+  } else {
+    for (int it = 0; it < iters; ++it) {
+      const int r0 = begin_step(it, rt);
+      const int nvalid = min(kBR, e - r0);
+      const bool vis = r0 + nvalid - 1 >= seer_first;
+      const int sp = (it + kDkvStages - 1) % kDkvStages, pb = (it - 1) & 1;
+      const char *dl = (const char *)sm.dout[it % kDkvStages];
+      // separate branches, each updating one accumulator set in place
+      if (vis_prev) ds_dp(sp, pb, dl, T_{}, F_{});
+      if (vis) ds_dp(sp, pb, dl, F_{}, T_{});
+      vis_prev = vis;
+    }
+    // finish the last tile once its P is in LDS
+    lds_barrier();
+    if (vis_prev)
+      ds_dp((iters - 1) % kDkvStages, (iters - 1) & 1, (const char *)sm.dout[0], T_{}, F_{});
   }
-  // the dS waves finish the last tile once its P is in LDS
-  lds_barrier();
-  if (!pwave && vis_prev) ds_step((iters - 1) % kDkvStages, (iters - 1) & 1);
 
-  const int key = kw0 + l32;
   if (!wactive || key >= e) return;
   float *out = (pwave ? a.dv : a.dk) + ((int64_t)key * a.hkv + kvh) * D + hf * 4;
   const float mul = pwave ? 1.f : a.scale;
