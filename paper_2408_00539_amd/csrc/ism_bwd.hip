@@ -9,7 +9,7 @@
 //  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji).
 //  3. dK/dV kernel, key-tile outer: a workgroup owns 128 keys of one KV head
 //     (32 per wave pair, lane <-> key), walks the query heads of the group
-//     and the 32-row tiles from seer[first key] to the dialogue end, and
+//     and the 64-row tiles from seer[first key] to the dialogue end, and
 //     accumulates dV^T += dO^T P and dK^T += Q^T dS with P = exp(S - LSE),
 //     dS = P o (dP - delta), dP = dO V^T. Q and dO tiles are staged in LDS
 //     row-major; the products over rows read them through transposing reads.
@@ -17,8 +17,6 @@
 //     S^T and dP^T per 64-key tile and accumulates dQ^T += K^T dS^T.
 // All products are bf16 MFMA 32x32x16 with fp32 accumulation; gradients are
 // written in fp32.
-#include <type_traits>
-
 #include "ism_common.h"
 #include "ism_kernels.h"
 
@@ -33,7 +31,7 @@ namespace ism {
 
 namespace {
 
-constexpr int kBR = 32;   // rows per tile in the dK/dV kernel
+constexpr int kBR = 64;   // rows per tile in the dK/dV kernel
 constexpr int kKW = 128;  // keys per dK/dV workgroup (32 per wave)
 constexpr int kBK = 64;   // keys per tile in the dQ kernel
 
@@ -85,60 +83,29 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 // ---------------------------------------------------------------- dK / dV
 
 // Ring of Q / dO tile stages: the tile a dS wave finishes (t - 1), the
-// current tile t, and tiles t + 1, t + 2 in flight.
-constexpr int kDkvStages = 4;
+// current tile t, and tile t + 1 in flight.
+constexpr int kDkvStages = 3;
 
-// Q and dO tiles of 32 rows (unpadded swizzled rows, see swz<D>()) plus the
+// Q and dO tiles of 64 rows (unpadded swizzled rows, see swz<D>()) plus the
 // per-row LSE (log2 units) and delta, all filled by direct global->LDS
-// transfers; and P of the last two tiles for each wave pair, fp32 in MFMA
-// accumulator layout (lane-private, 16 values per lane, stored as 4 x 16
-// bytes so that consecutive lanes touch consecutive bytes).
+// transfers; and P of the last two tiles for each wave pair in the bf16 B
+// operand form of the dV product (lane-private, 4 x 16 bytes per lane, laid
+// out so that consecutive lanes touch consecutive bytes).
 template <int D>
 struct DkvSmem {
   bf16_t q[kDkvStages][kBR * D];
   bf16_t dout[kDkvStages][kBR * D];
   __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
   __attribute__((aligned(16))) float delta[kDkvStages][kBR];
-  __attribute__((aligned(16))) float p[2][4][16 * 64];
+  __attribute__((aligned(16))) u32x4 p[2][4][4 * 64];
 };
 
-// 32 consecutive 4-byte values base[min(r0 + l, last)], l < 32, to lds[l]
-// through one global_load_lds_dword (lanes 32..63 idle).
+// 64 consecutive 4-byte values base[min(r0 + l, last)] to lds[l] through one
+// global_load_lds_dword.
 __device__ __forceinline__ void dma_row_scalars(const void *base, int r0, int last, void *lds,
                                                 int lane) {
-  const uint32_t lb = lds_addr(lds);
-  if (lane < 32) {
-    const int r = min(r0 + lane, last);
-    dma_x1((const char *)base + (int64_t)r * 4, lb);
-  }
-}
-
-// s_waitcnt vmcnt(n) with expcnt / lgkmcnt left unconstrained.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
-  switch (n) {
-    case 0: wait_vmcnt<0>(); break;
-    case 1: wait_vmcnt<1>(); break;
-    case 2: wait_vmcnt<2>(); break;
-    default: wait_vmcnt<3>(); break;
-  }
-}
-
-// fr[bt] slots of the B operand (16 rows x 32 keys) from four accumulator
-// row groups: accumulator rows 8i..8i+3 (+4 for the upper half-wave) are
-// slots 4 (i & 1) .. of operand i >> 1, matching the k order of the
-// transposing A-operand reads.
-__device__ __forceinline__ void put_rows(bf16x8 (&fr)[2], int i, f32x2 lo, f32x2 hi) {
-  const int bt = i >> 1, sl = (i & 1) * 2;
-  u32x4 x = __builtin_bit_cast(u32x4, fr[bt]);
-  x[sl] = cvt_bf16x2(lo);
-  x[sl + 1] = cvt_bf16x2(hi);
-  fr[bt] = __builtin_bit_cast(bf16x8, x);
+  const int r = min(r0 + lane, last);
+  dma_x1((const char *)base + (int64_t)r * 4, lds_addr(lds));
 }
 
 // N products in a fixed order: product n consumes operand n, read from LDS
@@ -162,27 +129,31 @@ __device__ __forceinline__ void product_stream(Rd &&rd, Mm &&mm, Mid &&mid) {
 }
 
 // Eight waves in four pairs; pair p owns the 32 keys c0 + 32 p (lane <->
-// key) and its two waves share one SIMD:
-//  * the P wave (p) computes S = Q K^T and P = exp(S - LSE) (masked) for
-//    tile t, accumulates dV^T += dO^T P and leaves P in LDS;
+// key) and its two waves share one SIMD. Per 64-row tile t:
+//  * the P wave (p) computes S = Q K^T and P = exp(S - LSE) (masked),
+//    accumulates dV^T += dO^T P and leaves P (bf16) in LDS;
 //  * the dS wave (p + 4), one tile behind, forms dS = P o (dP - delta) with
 //    its partner's P and accumulates dK^T += Q^T dS, then computes
 //    dP = dO V^T of tile t for the next step.
-// Each wave does 16 of the 32 products per tile with no product computed
+// Each wave does 32 of the 64 products per tile with no product computed
 // twice, and the exp / elementwise phase of one wave of a pair falls in the
-// other's MFMA phase. Visibility needs no per-row bounds: row r sees key i
-// exactly when r >= seer[i] (seer is non-decreasing in i).
+// other's MFMA phase. Accumulator element r = 4i + j of row block rb holds
+// row 32 rb + 8i + 4h + j (h = lane / 32), so bf16 operand kk = 2 rb + bt of
+// the products over rows is simply elements 8 bt .. 8 bt + 7 of block rb.
+// Visibility needs no per-row bounds: row r sees key i exactly when
+// r >= seer[i] (seer is non-decreasing in i).
 template <int D>
 __global__ void __launch_bounds__(512)
 __attribute__((amdgpu_waves_per_eu(ISM_DKV_WPE, ISM_DKV_WPE)))
 dkv_kernel(BwdArgs a, int ktiles) {
   constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2, LA = 3;
+  constexpr int NRB = kBR / 32, NKK = kBR / 16;  // 32-row blocks, 16-row k steps
   __shared__ DkvSmem<D> sm;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int pair = wave & 3;
   const bool pwave = wave < 4;
-  const int l32 = lane & 31, hf = lane >> 5;
+  const int hf = lane >> 5;
 
   // (dialogue, KV head) groups run on one XCD each; early key tiles (the
   // longest row ranges) first.
@@ -203,7 +174,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
   // first rows that see the wave's first and last key, and this lane's key
   const int seer_first = wactive ? a.seer[kw0] : e;
   const int seer_last = (wactive && kw0 + 31 < e) ? a.seer[kw0 + 31] : e;
-  const int key = kw0 + l32;
+  const int key = kw0 + (lane & 31);
   const int seer_k = key < e ? a.seer[key] : 0x7fffffff;
 
   // B operands of this wave's products: K (P wave, for S) or V (dS wave,
@@ -220,7 +191,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
-  f32x16 dp = {};         // dS wave: dP of the previous tile
+  f32x16 dp[NRB];         // dS wave: dP of the previous tile
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) dp[rb] = f32x16{};
   bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   const int rstart = a.seer[c0];
@@ -229,11 +202,8 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int64_t rs = (int64_t)a.hq * D;
   DmaTile<D, kBR, 8> dma;
   dma.init(tid, rs);
-  SwzOffsets<D> so;
+  SwzBases<D> so;
   so.init(lane);
-  // transfers this wave issues per tile: Q and dO blocks, plus one row-scalar
-  // array for waves 6 and 7
-  const int my_ops = 2 * (wave < DmaTile<D, kBR, 8>::T ? 1 : 0) + (wave >= 6 ? 1 : 0);
   // next tile to transfer: index, head, row tile
   int nx = 0, nx_h = kvh * G, nx_rt = 0;
   auto issue_next = [&]() {
@@ -248,109 +218,124 @@ dkv_kernel(BwdArgs a, int ktiles) {
   };
 
   // dS wave: dS = P o (dP - delta) for the previous tile (stage sp, P buffer
-  // pbuf), dK^T[d][key] += Q^T[d][row] dS[row][key]; then, if dl is set,
-  // dP[row][key] = dO V^T of the current tile.
-  auto ds_dp = [&](int sp, int pbuf, const char *dl, auto has_ds, auto has_dp) {
-    constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
-    constexpr int NK = DS ? 2 * NDB : 0, N = NK + (DP ? NKS : 0);
+  // pbuf), dK^T[d][key] += Q^T[d][row] dS[row][key]; or dP[row][key] =
+  // dO V^T of the current tile (stage st).
+  auto ds_dk = [&](int sp, int pbuf) {
     const char *ql = (const char *)sm.q[sp];
-    const float *pp = sm.p[pbuf][pair];
-    f32x4 pv[4], dlt[4];
-    if (DS) {
+    const u32x4 *pp = sm.p[pbuf][pair];
+    u32x4 pw[NKK];
+    f32x4 dlt[NRB][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pv[i] = *(const f32x4 *)(pp + (i * 64 + lane) * 4);
-        dlt[i] = *(const f32x4 *)&sm.delta[sp][8 * i + 4 * hf];
-      }
-    }
-    bf16x8 fr[2] = {};
-    auto rd = [&](int n) -> bf16x8 {
-      if (n < NK) {
-        const uint32_t o = 16 * (n & 1) * RB;
-        return tr_operand_at(ql, o + so.trk[n >> 1][0], o + so.trk[n >> 1][1]);
-      }
-      return *(const bf16x8 *)(dl + so.rowk[n - NK]);
+    for (int kk = 0; kk < NKK; ++kk) pw[kk] = pp[kk * 64 + lane];
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dlt[rb][i] = *(const f32x4 *)&sm.delta[sp][32 * rb + 8 * i + 4 * hf];
+    bf16x8 fr[NKK];
+    auto rd = [&](int n) -> bf16x8 {  // n = kk * NDB + db
+      const int kk = n / NDB, db = n % NDB;
+      const uint32_t o = 16 * kk * RB;
+      return tr_operand_at(ql, o + so.tr(db, 0), o + so.tr(db, 1));
     };
-    f32x16 dpn;
     auto mm = [&](int n, bf16x8 x) {
-      if (n < NK) {
-        acc[n >> 1] = mfma32x32x16(x, fr[n & 1], acc[n >> 1]);
-      } else {
-        const int ks = n - NK;
-        dpn = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dpn);
-      }
+      const int kk = n / NDB, db = n % NDB;
+      acc[db] = mfma32x32x16(x, fr[kk], acc[db]);
     };
     auto mid = [&]() {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x2 w[2];
+      for (int kk = 0; kk < NKK; ++kk) {
+        const int rb = kk >> 1, bt = kk & 1;
+        u32x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j >> 1][j & 1] = pv[i][j] * (dp[4 * i + j] - dlt[i][j]);
-        put_rows(fr, i, w[0], w[1]);
+        for (int u = 0; u < 4; ++u) {
+          const int e0 = 8 * bt + 2 * u;  // accumulator elements e0, e0 + 1
+          f32x2 x;
+          x[0] = bf16_lo(pw[kk][u]) * (dp[rb][e0] - dlt[rb][e0 >> 2][e0 & 3]);
+          x[1] = bf16_hi(pw[kk][u]) * (dp[rb][e0 + 1] - dlt[rb][e0 >> 2][(e0 & 3) + 1]);
+          w[u] = cvt_bf16x2(x);
+        }
+        fr[kk] = __builtin_bit_cast(bf16x8, w);
       }
     };
-    product_stream<N, DS ? 0 : -1, LA>(rd, mm, mid);
-    if (DP) dp = dpn;
+    product_stream<NKK * NDB, 0, LA>(rd, mm, mid);
+  };
+  auto dp_tile = [&](int st) {
+    const char *dl = (const char *)sm.dout[st];
+    auto rd = [&](int n) -> bf16x8 {  // n = ks * NRB + rb
+      return *(const bf16x8 *)(dl + (n % NRB) * 32 * RB + so.row(n / NRB));
+    };
+    auto mm = [&](int n, bf16x8 x) {
+      const int ks = n / NRB, rb = n % NRB;
+      dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dp[rb]);
+    };
+    product_stream<NKS * NRB, -1, LA>(rd, mm, [] {});
   };
 
   // P wave on the current tile (stage st, rows r0.., nvalid valid): S, P
-  // (masked unless every row sees every key) to LDS and into operand form,
+  // (masked unless every row sees every key) to LDS in operand form,
   // dV^T += dO^T P.
   auto p_dv = [&](int st, int r0, int nvalid, int pbuf, bool full) {
     const char *ql = (const char *)sm.q[st];
     const char *dl = (const char *)sm.dout[st];
-    f32x4 l2[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) l2[i] = *(const f32x4 *)&sm.lse2[st][8 * i + 4 * hf];
-    float *pp = sm.p[pbuf][pair];
-    f32x16 sacc;
-    bf16x8 fr[2] = {};
+    u32x4 *pp = sm.p[pbuf][pair];
+    f32x16 sacc[NRB];
+    bf16x8 fr[NKK];
+    constexpr int NS = NKS * NRB;
     auto rd = [&](int n) -> bf16x8 {
-      if (n < NKS) return *(const bf16x8 *)(ql + so.rowk[n]);
-      const int j = n - NKS;
-      const uint32_t o = 16 * (j & 1) * RB;
-      return tr_operand_at(dl, o + so.trk[j >> 1][0], o + so.trk[j >> 1][1]);
+      if (n < NS) return *(const bf16x8 *)(ql + (n % NRB) * 32 * RB + so.row(n / NRB));
+      const int j = n - NS, kk = j / NDB, db = j % NDB;  // j = kk * NDB + db
+      const uint32_t o = 16 * kk * RB;
+      return tr_operand_at(dl, o + so.tr(db, 0), o + so.tr(db, 1));
     };
     auto mm = [&](int n, bf16x8 x) {
-      if (n < NKS) {
-        sacc = mfma32x32x16(x, bop[n], n == 0 ? f32x16{} : sacc);
+      if (n < NS) {
+        const int ks = n / NRB, rb = n % NRB;
+        sacc[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : sacc[rb]);
       } else {
-        const int j = n - NKS;
-        acc[j >> 1] = mfma32x32x16(x, fr[j & 1], acc[j >> 1]);
+        const int j = n - NS, kk = j / NDB, db = j % NDB;
+        acc[db] = mfma32x32x16(x, fr[kk], acc[db]);
       }
     };
     auto mid = [&]() {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 pv;
+      for (int rb = 0; rb < NRB; ++rb) {
+        f32x16 pv;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pv[j] = fast_exp2(fmaf(sacc[4 * i + j], sl2, -l2[i][j]));
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 l2 = *(const f32x4 *)&sm.lse2[st][32 * rb + 8 * i + 4 * hf];
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            pv[4 * i + j] = fast_exp2(fmaf(sacc[rb][4 * i + j], sl2, -l2[j]));
+        }
         if (!full) {
           // rows at or past nvalid repeat the last row (clamped transfers)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int rr = 8 * i + 4 * hf + j;
-            if (rr >= nvalid || r0 + rr < seer_k) pv[j] = 0.f;
+          for (int r = 0; r < 16; ++r) {
+            const int rr = 32 * rb + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (rr >= nvalid || r0 + rr < seer_k) pv[r] = 0.f;
           }
         }
-        *(f32x4 *)(pp + (i * 64 + lane) * 4) = pv;
-        put_rows(fr, i, f32x2{pv[0], pv[1]}, f32x2{pv[2], pv[3]});
+#pragma unroll
+        for (int bt = 0; bt < 2; ++bt) {
+          u32x4 w;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            w[u] = pack_bf16x2(pv[8 * bt + 2 * u], pv[8 * bt + 2 * u + 1]);
+          pp[(2 * rb + bt) * 64 + lane] = w;
+          fr[2 * rb + bt] = __builtin_bit_cast(bf16x8, w);
+        }
       }
     };
-    product_stream<NKS + 2 * NDB, NKS, LA>(rd, mm, mid);
+    product_stream<NS + NKK * NDB, NS, LA>(rd, mm, mid);
   };
 
-  using T_ = std::true_type;
-  using F_ = std::false_type;
   if (iters > 0) issue_next();
-  if (iters > 1) issue_next();
   // Start of step it (row tile rt): wait for its tile, synchronize, start
-  // the transfer of a later tile. Returns the tile's first row.
+  // the transfer of the next tile. Returns the tile's first row.
   auto begin_step = [&](int it, int &rt) {
     const int r0 = rstart + rt * kBR;
     if (++rt == nrt) rt = 0;
-    // tile it has landed once at most the next tile's transfers are pending
-    if (it + 1 < iters) wait_vmcnt_dyn(my_ops); else wait_vmcnt<0>();
+    wait_vmem();
     // Tile it visible to all waves; every wave is done with tile it - 2 and
     // with the P buffer the P waves write next. A bare s_barrier: the fences
     // of __syncthreads() would also drain the transfers still in flight.
@@ -374,17 +359,14 @@ dkv_kernel(BwdArgs a, int ktiles) {
       const int r0 = begin_step(it, rt);
       const int nvalid = min(kBR, e - r0);
       const bool vis = r0 + nvalid - 1 >= seer_first;
-      const int sp = (it + kDkvStages - 1) % kDkvStages, pb = (it - 1) & 1;
-      const char *dl = (const char *)sm.dout[it % kDkvStages];
       // separate branches, each updating one accumulator set in place
-      if (vis_prev) ds_dp(sp, pb, dl, T_{}, F_{});
-      if (vis) ds_dp(sp, pb, dl, F_{}, T_{});
+      if (vis_prev) ds_dk((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1);
+      if (vis) dp_tile(it % kDkvStages);
       vis_prev = vis;
     }
     // finish the last tile once its P is in LDS
     lds_barrier();
-    if (vis_prev)
-      ds_dp((iters - 1) % kDkvStages, (iters - 1) & 1, (const char *)sm.dout[0], T_{}, F_{});
+    if (vis_prev) ds_dk((iters - 1) % kDkvStages, (iters - 1) & 1);
   }
 
   if (!wactive || key >= e) return;

@@ -238,6 +238,28 @@ struct SwzOffsets {
   }
 };
 
+// The same offsets in compact form (3 registers instead of D/16 + D/8):
+// since the chunk index of k step ks is 2 ks + h and the d block db adds
+// 4 db to the chunk index, both enter the swizzled address only by XOR:
+// rowk[ks] = rowb ^ (ks << 5) and trk[db][s] = trb[s] ^ (db << 6) (the XOR
+// stays inside one tile row, whose byte offset is a multiple of 2 D).
+template <int D>
+struct SwzBases {
+  uint32_t rowb, trb[2];
+
+  __device__ __forceinline__ void init(int lane) {
+    SwzOffsets<D> o;
+    o.init(lane);
+    rowb = o.rowk[0];
+    trb[0] = o.trk[0][0];
+    trb[1] = o.trk[0][1];
+  }
+  __device__ __forceinline__ uint32_t row(int ks) const { return rowb ^ (uint32_t)(ks << 5); }
+  __device__ __forceinline__ uint32_t tr(int db, int s) const {
+    return trb[s] ^ (uint32_t)(db << 6);
+  }
+};
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) {
   return __builtin_bit_cast(float, w << 16);
 }
