@@ -393,13 +393,19 @@ struct DqSmem {
   bf16_t v[2][kBK * D];
 };
 
+// One wave owns 32 rows of one head (lane <-> row) and walks the 64-key
+// tiles its rows see. Per tile, in product order: S^T = K Q^T and dP^T =
+// V dO^T for keys 0-31, then for keys 32-63, then dQ^T += K^T dS^T for both
+// halves; the exponentials of each S^T half run beside the next dP^T
+// products and dS^T = P^T o (dP^T - delta) beside the products after that.
 template <int D>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_DQ_WPE, ISM_DQ_WPE)))
 dq_kernel(BwdArgs a, int hpw, int tiles) {
-  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2;
+  constexpr int NKS = D / 16, NDB = D / 32, RB = D * 2, LA = 3;
   __shared__ DqSmem<D> sm;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
 
   const int hsets = a.hq / hpw;
@@ -447,9 +453,10 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const bf16_t *vbase = (const bf16_t *)a.v + (int64_t)kvh * D;
   const int64_t rs = (int64_t)a.hkv * D;
   const int ntiles = (key_hi - s) / kBK + 1;
+  const int nw = active ? (wave_hi - s) / kBK + 1 : 0;  // this wave's tiles
   DmaTile<D, kBK> dma;
   dma.init(tid, rs);
-  SwzOffsets<D> so;
+  SwzBases<D> so;
   so.init(lane);
   const int64_t tile_elems = (int64_t)kBK * rs;
   const bf16_t *kt = kbase + (int64_t)s * rs;
@@ -458,6 +465,13 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   dma.issue(vt, rs, key_hi - s + 1, sm.v[0]);
   wait_vmem();
   __syncthreads();
+
+  // keys past the row's bound get P = 0 (score -inf)
+  auto mask = [&](f32x16 &x, int k0) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (k0 + (r >> 2) * 8 + hf * 4 + (r & 3) > lim_r) x[r] = -INFINITY;
+  };
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
@@ -468,49 +482,88 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       dma.issue(kt, rs, key_hi - (c0 + kBK) + 1, sm.k[buf ^ 1]);
       dma.issue(vt, rs, key_hi - (c0 + kBK) + 1, sm.v[buf ^ 1]);
     }
-    if (active && c0 <= wave_hi) {
+    if (t < nw) {
       const bool full = c0 + kBK - 1 <= wave_lo;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        // S^T[key][row], dP^T[key][row] for 32 keys, lane <-> row
-        f32x16 sacc, pacc;
-        const char *kl = (const char *)sm.k[buf];
-        const char *vl = (const char *)sm.v[buf];
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const uint32_t o = kb * 32 * RB + so.rowk[ks];
-          sacc = mfma32x32x16(*(const bf16x8 *)(kl + o), qf[ks], ks == 0 ? f32x16{} : sacc);
-          pacc = mfma32x32x16(*(const bf16x8 *)(vl + o), df[ks], ks == 0 ? f32x16{} : pacc);
+      const char *kl = (const char *)sm.k[buf];
+      const char *vl = (const char *)sm.v[buf];
+      // S^T / P^T and dP^T for the two 32-key halves; dS^T operands
+      f32x16 sc[2], pc[2];
+      u32x4 ds[2][2];
+      constexpr int NH = 2 * NKS;  // products per half (S^T and dP^T)
+      // products: [0, NH) S^T and dP^T half 0 (alternating), [NH, 2 NH) half 1,
+      // [2 NH, 2 NH + 4 NDB) dQ^T (kb, db, bt)
+      auto rd = [&](auto nc) -> bf16x8 {
+        constexpr int n = decltype(nc)::value;
+        if constexpr (n < 2 * NH) {
+          constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
+          return *(const bf16x8 *)(((m & 1) ? vl : kl) + kb * 32 * RB + so.row(ks));
+        } else {
+          constexpr int j = n - 2 * NH, kb = j / (2 * NDB), db = (j % (2 * NDB)) >> 1,
+                        bt = j & 1;
+          constexpr uint32_t o = (kb * 32 + 16 * bt) * RB;
+          return tr_operand_at(kl, o + so.tr(db, 0), o + so.tr(db, 1));
         }
-        bf16x8 dsf[2];
+      };
+      auto mm = [&](auto nc, bf16x8 x) {
+        constexpr int n = decltype(nc)::value;
+        if constexpr (n < 2 * NH) {
+          constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
+          if constexpr (m & 1) pc[kb] = mfma32x32x16(x, df[ks], ks == 0 ? f32x16{} : pc[kb]);
+          else sc[kb] = mfma32x32x16(x, qf[ks], ks == 0 ? f32x16{} : sc[kb]);
+        } else {
+          constexpr int j = n - 2 * NH, kb = j / (2 * NDB), db = (j % (2 * NDB)) >> 1,
+                        bt = j & 1;
+          dq[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, ds[kb][bt]), dq[db]);
+        }
+      };
+      // mask a finished S^T half just before its exponentials start
+      auto pre = [&](auto nc) {
+        constexpr int n = decltype(nc)::value;
+        if constexpr (n == NH) { if (!full) mask(sc[0], c0); }
+        if constexpr (n == 2 * NH) { if (!full) mask(sc[1], c0 + 32); }
+      };
+      // P^T and dS^T of half 0 in the slots of half 1's products (first the
+      // exponentials, then dS^T), of half 1 in the slots of half 0's dQ^T
+      // products, so that both are complete before the dQ^T products that
+      // read them
+      // (the empty asm keeps each result in its slot: IR passes would
+      // otherwise sink the work past the mask branch to its uses)
+      auto exp1 = [&](int kb, int r) {
+        float p = fast_exp2(fmaf(sc[kb][r], sl2, -lse2));
+        asm volatile("" : "+v"(p));
+        sc[kb][r] = p;
+      };
+      auto ds2 = [&](int kb, int r) {  // elements r, r + 1 (r even)
+        f32x2 x;
+        x[0] = sc[kb][r] * (pc[kb][r] - dlt);
+        x[1] = sc[kb][r + 1] * (pc[kb][r + 1] - dlt);
+        uint32_t w = cvt_bf16x2(x);
+        asm volatile("" : "+v"(w));
+        ds[kb][r >> 3][(r & 7) >> 1] = w;
+      };
+      auto work = [&](auto nc) {
+        constexpr int n = decltype(nc)::value;
+        if constexpr (n >= NH && n < 2 * NH) {
+          constexpr int E = 32 / NH, w = n - NH;  // element-steps per slot
+          if constexpr (w < NH / 2) {
 #pragma unroll
-        for (int bt = 0; bt < 2; ++bt) {
-          f32x2 w[4];
+            for (int c = 0; c < E; ++c) exp1(0, w * E + c);
+          } else {
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int r = 8 * bt + u;
-            float p = fast_exp2(fmaf(sacc[r], sl2, -lse2));
-            if (!full) {
-              const int key = c0 + kb * 32 + (r >> 2) * 8 + hf * 4 + (r & 3);
-              if (key > lim_r) p = 0.f;
-            }
-            w[u >> 1][u & 1] = p * (pacc[r] - dlt);
+            for (int c = 0; c < E; c += 2) ds2(0, (w - NH / 2) * E + c);
           }
-          u32x4 x;
+        } else if constexpr (n >= 2 * NH && n < 2 * NH + 2 * NDB) {
+          constexpr int E = 16 / NDB, w = n - 2 * NH;
+          if constexpr (w < NDB) {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) x[u] = cvt_bf16x2(w[u]);
-          dsf[bt] = __builtin_bit_cast(bf16x8, x);
-        }
+            for (int c = 0; c < E; ++c) exp1(1, w * E + c);
+          } else {
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-#pragma unroll
-          for (int bt = 0; bt < 2; ++bt) {
-            const uint32_t o = (kb * 32 + 16 * bt) * RB;
-            dq[db] = mfma32x32x16(tr_operand_at(kl, o + so.trk[db][0], o + so.trk[db][1]),
-                                  dsf[bt], dq[db]);
+            for (int c = 0; c < E; c += 2) ds2(1, (w - NDB) * E + c);
           }
         }
-      }
+      };
+      product_slots<2 * NH + 4 * NDB, LA>(rd, mm, pre, work);
     }
     wait_vmem();
     __syncthreads();

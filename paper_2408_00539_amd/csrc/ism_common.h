@@ -5,6 +5,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace ism {
 
 typedef __bf16 bf16_t;
@@ -259,6 +262,35 @@ struct SwzBases {
     return trb[s] ^ (uint32_t)(db << 6);
   }
 };
+
+// A fixed-order sequence of N MFMA products with compile-time slot indices
+// (each callback receives std::integral_constant<int, n>): before product n
+// pre(n); product n consumes operand n, which rd(n) read from LDS LA
+// products earlier; after it, work(n) (the vector work placed beside it).
+// Scheduling barriers between slots pin the order.
+template <int n, int N, int LA, class Rd, class Mm, class Pre, class Work>
+__device__ __forceinline__ void product_slot(bf16x8 *op, Rd &rd, Mm &mm, Pre &pre, Work &work) {
+  pre(std::integral_constant<int, n>{});
+  mm(std::integral_constant<int, n>{}, op[n]);
+  if constexpr (n + LA < N) op[n + LA] = rd(std::integral_constant<int, n + LA>{});
+  work(std::integral_constant<int, n>{});
+  __builtin_amdgcn_sched_barrier(0);
+}
+template <int n, int LA, class Rd>
+__device__ __forceinline__ void product_prefetch(bf16x8 *op, Rd &rd) {
+  if constexpr (n < LA) op[n] = rd(std::integral_constant<int, n>{});
+}
+template <int N, int LA, class Rd, class Mm, class Pre, class Work, int... Ns>
+__device__ __forceinline__ void product_slots_seq(Rd &rd, Mm &mm, Pre &pre, Work &work,
+                                                  std::integer_sequence<int, Ns...>) {
+  bf16x8 op[N];
+  (product_prefetch<Ns, LA>(op, rd), ...);
+  (product_slot<Ns, N, LA>(op, rd, mm, pre, work), ...);
+}
+template <int N, int LA, class Rd, class Mm, class Pre, class Work>
+__device__ __forceinline__ void product_slots(Rd &&rd, Mm &&mm, Pre &&pre, Work &&work) {
+  product_slots_seq<N, LA>(rd, mm, pre, work, std::make_integer_sequence<int, N>{});
+}
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) {
   return __builtin_bit_cast(float, w << 16);
