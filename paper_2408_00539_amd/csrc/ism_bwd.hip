@@ -217,118 +217,163 @@ dkv_kernel(BwdArgs a, int ktiles) {
     if (++nx_rt == nrt) { nx_rt = 0; ++nx_h; }
   };
 
-  // dS wave: dS = P o (dP - delta) for the previous tile (stage sp, P buffer
-  // pbuf), dK^T[d][key] += Q^T[d][row] dS[row][key]; or dP[row][key] =
-  // dO V^T of the current tile (stage st).
-  auto ds_dk = [&](int sp, int pbuf) {
+  // dS wave, one product stream per step: for the previous tile (stage sp,
+  // P buffer pbuf) dS = P o (dP - delta) in 16-row slices, each slice's
+  // dK^T[d][key] += Q^T[d][row] dS[row][key] products running beside the
+  // elementwise work of the next slice; then (DP) dP[row][key] = dO V^T of
+  // the current tile (stage st). The empty asm statements keep each slot's
+  // vector work in its slot (IR passes would otherwise sink it to its use).
+  auto ds_dp = [&](int sp, int pbuf, int st, auto has_ds, auto has_dp) {
+    constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
+    constexpr int NK = DS ? NKK * NDB : 0, N = NK + (DP ? NKS * NRB : 0);
     const char *ql = (const char *)sm.q[sp];
+    const char *dl = (const char *)sm.dout[st];
     const u32x4 *pp = sm.p[pbuf][pair];
     u32x4 pw[NKK];
     f32x4 dlt[NRB][4];
+    if constexpr (DS) {
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) pw[kk] = pp[kk * 64 + lane];
+      for (int kk = 0; kk < NKK; ++kk) pw[kk] = pp[kk * 64 + lane];
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb)
+      for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dlt[rb][i] = *(const f32x4 *)&sm.delta[sp][32 * rb + 8 * i + 4 * hf];
-    bf16x8 fr[NKK];
-    auto rd = [&](int n) -> bf16x8 {  // n = kk * NDB + db
-      const int kk = n / NDB, db = n % NDB;
-      const uint32_t o = 16 * kk * RB;
-      return tr_operand_at(ql, o + so.tr(db, 0), o + so.tr(db, 1));
+        for (int i = 0; i < 4; ++i)
+          dlt[rb][i] = *(const f32x4 *)&sm.delta[sp][32 * rb + 8 * i + 4 * hf];
+    }
+    u32x4 fw[NKK];
+    // dS elements 2u, 2u + 1 of slice kk (accumulator elements 8 bt + 2u ..)
+    auto ds_pair = [&](int kk, int u) {
+      const int rb = kk >> 1, e0 = 8 * (kk & 1) + 2 * u;
+      f32x2 x;
+      x[0] = bf16_lo(pw[kk][u]) * (dp[rb][e0] - dlt[rb][e0 >> 2][e0 & 3]);
+      x[1] = bf16_hi(pw[kk][u]) * (dp[rb][e0 + 1] - dlt[rb][e0 >> 2][(e0 & 3) + 1]);
+      uint32_t w = cvt_bf16x2(x);
+      asm volatile("" : "+v"(w));
+      fw[kk][u] = w;
     };
-    auto mm = [&](int n, bf16x8 x) {
-      const int kk = n / NDB, db = n % NDB;
-      acc[db] = mfma32x32x16(x, fr[kk], acc[db]);
-    };
-    auto mid = [&]() {
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const int rb = kk >> 1, bt = kk & 1;
-        u32x4 w;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e0 = 8 * bt + 2 * u;  // accumulator elements e0, e0 + 1
-          f32x2 x;
-          x[0] = bf16_lo(pw[kk][u]) * (dp[rb][e0] - dlt[rb][e0 >> 2][e0 & 3]);
-          x[1] = bf16_hi(pw[kk][u]) * (dp[rb][e0 + 1] - dlt[rb][e0 >> 2][(e0 & 3) + 1]);
-          w[u] = cvt_bf16x2(x);
-        }
-        fr[kk] = __builtin_bit_cast(bf16x8, w);
+    auto rd = [&](auto nc) -> bf16x8 {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n < NK) {  // n = kk * NDB + db
+        constexpr int kk = n / NDB, db = n % NDB;
+        return tr_operand_at(ql, 16 * kk * RB + so.tr(db, 0), 16 * kk * RB + so.tr(db, 1));
+      } else {  // n - NK = ks * NRB + rb
+        constexpr int j = n - NK;
+        return *(const bf16x8 *)(dl + (j % NRB) * 32 * RB + so.row(j / NRB));
       }
     };
-    product_stream<NKK * NDB, 0, LA>(rd, mm, mid);
-  };
-  auto dp_tile = [&](int st) {
-    const char *dl = (const char *)sm.dout[st];
-    auto rd = [&](int n) -> bf16x8 {  // n = ks * NRB + rb
-      return *(const bf16x8 *)(dl + (n % NRB) * 32 * RB + so.row(n / NRB));
+    auto mm = [&](auto nc, bf16x8 x) {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n < NK) {
+        constexpr int kk = n / NDB, db = n % NDB;
+        acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
+      } else {
+        constexpr int j = n - NK, ks = j / NRB, rb = j % NRB;
+        dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dp[rb]);
+      }
     };
-    auto mm = [&](int n, bf16x8 x) {
-      const int ks = n / NRB, rb = n % NRB;
-      dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dp[rb]);
+    auto pre = [&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (DS && n == 0) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) ds_pair(0, u);
+      }
     };
-    product_stream<NKS * NRB, -1, LA>(rd, mm, [] {});
+    auto work = [&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      // slice kk + 1 during the NDB products of slice kk
+      if constexpr (DS && n < NK - NDB) {
+        constexpr int kk = n / NDB + 1, w = n % NDB, per = 4 / NDB;
+#pragma unroll
+        for (int c = 0; c < per; ++c) ds_pair(kk, w * per + c);
+      }
+    };
+    product_slots<N, LA>(rd, mm, pre, work);
   };
 
-  // P wave on the current tile (stage st, rows r0.., nvalid valid): S, P
-  // (masked unless every row sees every key) to LDS in operand form,
-  // dV^T += dO^T P.
+  // P wave on the current tile (stage st, rows r0.., nvalid valid), one
+  // product stream: S of row block 0, S of row block 1 beside the
+  // exponentials of block 0, dV^T += dO^T P for block 0 beside the
+  // exponentials of block 1, then dV for block 1. P goes to LDS (and into
+  // operand form) in 16-row slices; rows are masked unless every row sees
+  // every key.
   auto p_dv = [&](int st, int r0, int nvalid, int pbuf, bool full) {
     const char *ql = (const char *)sm.q[st];
     const char *dl = (const char *)sm.dout[st];
     u32x4 *pp = sm.p[pbuf][pair];
     f32x16 sacc[NRB];
-    bf16x8 fr[NKK];
-    constexpr int NS = NKS * NRB;
-    auto rd = [&](int n) -> bf16x8 {
-      if (n < NS) return *(const bf16x8 *)(ql + (n % NRB) * 32 * RB + so.row(n / NRB));
-      const int j = n - NS, kk = j / NDB, db = j % NDB;  // j = kk * NDB + db
-      const uint32_t o = 16 * kk * RB;
-      return tr_operand_at(dl, o + so.tr(db, 0), o + so.tr(db, 1));
+    u32x4 fw[NKK];
+    f32x4 l2[NRB][4];
+    constexpr int NS = NKS * NRB;  // S products, row-block major
+    constexpr int EPS = 16 / NKS;  // exponentials per slot
+    auto rd = [&](auto nc) -> bf16x8 {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n < NS) {
+        return *(const bf16x8 *)(ql + (n / NKS) * 32 * RB + so.row(n % NKS));
+      } else {  // n - NS = kk * NDB + db
+        constexpr int kk = (n - NS) / NDB, db = (n - NS) % NDB;
+        return tr_operand_at(dl, 16 * kk * RB + so.tr(db, 0), 16 * kk * RB + so.tr(db, 1));
+      }
     };
-    auto mm = [&](int n, bf16x8 x) {
-      if (n < NS) {
-        const int ks = n / NRB, rb = n % NRB;
+    auto mm = [&](auto nc, bf16x8 x) {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n < NS) {
+        constexpr int rb = n / NKS, ks = n % NKS;
         sacc[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : sacc[rb]);
       } else {
-        const int j = n - NS, kk = j / NDB, db = j % NDB;
-        acc[db] = mfma32x32x16(x, fr[kk], acc[db]);
+        constexpr int kk = (n - NS) / NDB, db = (n - NS) % NDB;
+        acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
       }
     };
-    auto mid = [&]() {
+    auto mask_rb = [&](int rb) {
+      // rows at or past nvalid repeat the last row (clamped transfers)
 #pragma unroll
-      for (int rb = 0; rb < NRB; ++rb) {
-        f32x16 pv;
+      for (int r = 0; r < 16; ++r) {
+        const int rr = 32 * rb + 8 * (r >> 2) + 4 * hf + (r & 3);
+        if (rr >= nvalid || r0 + rr < seer_k) sacc[rb][r] = -INFINITY;
+      }
+    };
+    auto pre = [&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n == 0) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x4 l2 = *(const f32x4 *)&sm.lse2[st][32 * rb + 8 * i + 4 * hf];
+        for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            pv[4 * i + j] = fast_exp2(fmaf(sacc[rb][4 * i + j], sl2, -l2[j]));
-        }
-        if (!full) {
-          // rows at or past nvalid repeat the last row (clamped transfers)
+          for (int i = 0; i < 4; ++i)
+            l2[rb][i] = *(const f32x4 *)&sm.lse2[st][32 * rb + 8 * i + 4 * hf];
+      }
+      if constexpr (n == NKS || n == 2 * NKS) {
+        if (!full) mask_rb(n / NKS - 1);
+      }
+    };
+    // exponentials of block rb in the NKS slots after its S is complete;
+    // each finished 16-row slice goes to LDS and operand form
+    auto work = [&](auto nc) {
+      constexpr int n = decltype(nc)::value;
+      if constexpr (n >= NKS && n < 3 * NKS) {
+        constexpr int rb = n / NKS - 1, w = n % NKS;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int rr = 32 * rb + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (rr >= nvalid || r0 + rr < seer_k) pv[r] = 0.f;
-          }
-        }
-#pragma unroll
-        for (int bt = 0; bt < 2; ++bt) {
-          u32x4 w;
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            w[u] = pack_bf16x2(pv[8 * bt + 2 * u], pv[8 * bt + 2 * u + 1]);
-          pp[(2 * rb + bt) * 64 + lane] = w;
-          fr[2 * rb + bt] = __builtin_bit_cast(bf16x8, w);
+        for (int c = 0; c < EPS; c += 2) {
+          const int e0 = w * EPS + c;  // accumulator elements e0, e0 + 1
+          f32x2 x;
+          x[0] = fast_exp2(fmaf(sacc[rb][e0], sl2, -l2[rb][e0 >> 2][e0 & 3]));
+          x[1] = fast_exp2(fmaf(sacc[rb][e0 + 1], sl2, -l2[rb][e0 >> 2][(e0 & 3) + 1]));
+          uint32_t p2 = cvt_bf16x2(x);
+          asm volatile("" : "+v"(p2));
+          fw[2 * rb + (e0 >> 3)][(e0 & 7) >> 1] = p2;
+          if ((e0 & 7) == 6) pp[(2 * rb + (e0 >> 3)) * 64 + lane] = fw[2 * rb + (e0 >> 3)];
         }
       }
     };
-    product_stream<NS + NKK * NDB, NS, LA>(rd, mm, mid);
+    product_slots<NS + NKK * NDB, LA>(rd, mm, pre, work);
   };
 
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  // Zero the LDS once: the dS waves' first step reads a P buffer, delta and
+  // Q stage that no tile has filled yet (and multiplies them by zeros).
+  for (int i = tid; i < (int)(sizeof(DkvSmem<D>) / 16); i += 512)
+    ((u32x4 *)&sm)[i] = u32x4{};
+  __syncthreads();
   if (iters > 0) issue_next();
   // Start of step it (row tile rt): wait for its tile, synchronize, start
   // the transfer of the next tile. Returns the tile's first row.
@@ -350,7 +395,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
     for (int it = 0; it < iters; ++it) {
       const int r0 = begin_step(it, rt);
       const int nvalid = min(kBR, e - r0);
-      if (r0 + nvalid - 1 < seer_first) continue;  // no row sees these keys
+      if (r0 + nvalid - 1 < seer_first) {  // no row sees these keys: P = 0
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) sm.p[it & 1][pair][kk * 64 + lane] = u32x4{};
+        continue;
+      }
       p_dv(it % kDkvStages, r0, nvalid, it & 1, nvalid == kBR && r0 >= seer_last);
     }
     lds_barrier();
@@ -359,14 +408,16 @@ dkv_kernel(BwdArgs a, int ktiles) {
       const int r0 = begin_step(it, rt);
       const int nvalid = min(kBR, e - r0);
       const bool vis = r0 + nvalid - 1 >= seer_first;
-      // separate branches, each updating one accumulator set in place
-      if (vis_prev) ds_dk((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1);
-      if (vis) dp_tile(it % kDkvStages);
+      (void)vis;
+      // one stream per step: an invisible previous tile has P = 0 in LDS, so
+      // its dK products add nothing; an invisible current tile's dP is
+      // never used
+      ds_dp((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1, it % kDkvStages, T_{}, T_{});
       vis_prev = vis;
     }
     // finish the last tile once its P is in LDS
     lds_barrier();
-    if (vis_prev) ds_dk((iters - 1) % kDkvStages, (iters - 1) & 1);
+    if (vis_prev) ds_dp((iters - 1) % kDkvStages, (iters - 1) & 1, 0, T_{}, F_{});
   }
 
   if (!wactive || key >= e) return;
