@@ -273,6 +273,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
     };
     auto pre = [&](auto nc) {
       constexpr int n = decltype(nc)::value;
+      if constexpr (n == 2) {
+        if (nx < iters) issue_next();
+      }
       if constexpr (DS && n == 0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) ds_pair(0, u);
@@ -334,6 +337,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
     };
     auto pre = [&](auto nc) {
       constexpr int n = decltype(nc)::value;
+      if constexpr (n == 2) {
+        if (nx < iters) issue_next();
+      }
       if constexpr (n == 0) {
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb)
@@ -375,8 +381,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
     ((u32x4 *)&sm)[i] = u32x4{};
   __syncthreads();
   if (iters > 0) issue_next();
-  // Start of step it (row tile rt): wait for its tile, synchronize, start
-  // the transfer of the next tile. Returns the tile's first row.
+  // Start of step it (row tile rt): wait for its tile and synchronize; the
+  // transfer of the next tile starts a few products into the step's product
+  // stream (off the path to the first product). Returns the tile's first row.
   auto begin_step = [&](int it, int &rt) {
     const int r0 = rstart + rt * kBR;
     if (++rt == nrt) rt = 0;
@@ -385,7 +392,6 @@ dkv_kernel(BwdArgs a, int ktiles) {
     // with the P buffer the P waves write next. A bare s_barrier: the fences
     // of __syncthreads() would also drain the transfers still in flight.
     lds_barrier();
-    if (nx < iters) issue_next();
     return r0;
   };
   // The two roles run separate loops (same barrier count) so that each
@@ -398,6 +404,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if (r0 + nvalid - 1 < seer_first) {  // no row sees these keys: P = 0
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) sm.p[it & 1][pair][kk * 64 + lane] = u32x4{};
+        if (nx < iters) issue_next();
         continue;
       }
       p_dv(it % kDkvStages, r0, nvalid, it & 1, nvalid == kBR && r0 >= seer_last);
