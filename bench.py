@@ -1,11 +1,11 @@
 """Benchmark of the ISM attention hot path on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                [--only step|all]
+                [--only step|all] [--calibrate-copy]
 
 A step is one training pass of the attention hot path over one batch of
 workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
-visibility prep, the forward and, once built, the backward. ``value`` is the
+visibility prep, the forward and the backward. ``value`` is the
 useful (unmasked) TFLOP/s of that step: 4*d FLOPs per visible (row, key) pair
 and query head for the forward, 10*d for the backward. The other paths of the
 hot path are measured on their own workloads and reported under ``paths``:
@@ -13,6 +13,13 @@ the grouped-KV forward (workload 2), the cached prefill and the decode stream
 (workload 3), the backward (workload 4).
 
 The last line of stdout is one JSON object; everything else goes to stderr.
+
+``roofline.traffic`` (HBM bytes per launch of the backward) comes from the
+FETCH_SIZE / WRITE_SIZE counter runs recorded in
+``profiles/traffic_step_8x4096_h32_d128.json``, scaled by what the same
+counters read for a plain copy of known size (``--calibrate-copy`` runs that
+copy); it is reported only while the kernel sources hash to the value
+recorded with the counters, else null.
 """
 
 from __future__ import annotations
@@ -32,6 +39,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = ("ISM attention useful TFLOP/s (fwd, bwd) and % bf16 MFMA peak; "
           "decode HBM GB/s")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_step_8x4096_h32_d128.json")
+COPY_BYTES = 1 << 30  # --calibrate-copy: bytes read (and written) per copy
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
 
@@ -218,6 +227,44 @@ def _cpu_model():
     return platform.processor()
 
 
+def kernel_source_hash():
+    """sha256 over the library's kernel sources (names and contents)."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2408_00539_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per backward launch from the committed counter record, or
+    None when there is none or the kernels changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return rec.get("bwd_bytes_per_launch")
+
+
+def calibrate_copy():
+    """A plain device copy of COPY_BYTES, ten times (for the counter scale)."""
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "copies": 10}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -225,6 +272,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["step", "all"], default="all")
+    ap.add_argument("--calibrate-copy", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU "
@@ -238,8 +286,11 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     ops.lib()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     timer = Timer()
-    with_bwd = _bwd_available()
+    with_bwd = True
 
     log("generating workload 1 ...")
     w1 = W.make_workload(1)
@@ -301,31 +352,12 @@ def main():
                      "achieved": round(dom["tflops"], 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(dom["tflops"] / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": recorded_traffic() if with_bwd else None},
         "cpu_baseline": cpu,
         "paths": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                       for kk, vv in v.items()} for k, v in paths.items()},
     }
     print(json.dumps(line), flush=True)
-
-
-def _bwd_available():
-    """True once the backward entry point runs on this build."""
-    import torch
-    from paper_2408_00539_amd import ops, workloads as W
-    segs_h = W.segments_from_lengths([[(4, True)]])
-    segs = ops.Segments.from_host(segs_h.cu_seqlens, segs_h.cu_segs,
-                                  segs_h.seg_is_query)
-    x = torch.zeros((4, 1, 64), dtype=torch.bfloat16, device="cuda")
-    lse = torch.zeros((1, 4), dtype=torch.float32, device="cuda")
-    try:
-        ops.bwd(x, x, x, x, lse, x, segs)
-        torch.cuda.synchronize()
-        return True
-    except ops.IsmError as e:
-        if e.status == 3:
-            return False
-        raise
 
 
 if __name__ == "__main__":
