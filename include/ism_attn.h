@@ -132,8 +132,9 @@ ism_status ism_attn_prefill_cached(
  * parallel and merged exactly (0 = choose automatically). o [batch, hq, d]
  * bf16; lse [hq, batch] fp32 or NULL. The caller guarantees p_b < cache_cap
  * and advances cache_seqlens by 1 afterwards. max_seqlen bounds p_b + 1 for
- * the split choice (0 = cache_cap). Workspace: ISM_OP_DECODE with the same
- * num_splits. */
+ * the split choice (0 = cache_cap). Workspace: ism_attn_workspace_size(
+ * ISM_OP_DECODE, batch, 0, max_seqlen (with 0 replaced by cache_cap), hq,
+ * hkv, d, num_splits). */
 ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            void *k_cache, void *v_cache, int32_t cache_cap,
                            const int32_t *cache_seqlens, int32_t batch,
