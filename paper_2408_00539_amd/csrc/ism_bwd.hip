@@ -97,7 +97,7 @@ struct DkvSmem {
   bf16_t dout[kDkvStages][kBR * D];
   __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
   __attribute__((aligned(16))) float delta[kDkvStages][kBR];
-  __attribute__((aligned(16))) u32x4 p[2][4][4 * 64];
+  __attribute__((aligned(16))) u32x4 p[kDkvStages][4][4 * 64];
 };
 
 // 64 consecutive 4-byte values base[min(r0 + l, last)] to lds[l] through one
@@ -204,10 +204,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
   dma.init(tid, rs);
   SwzBases<D> so;
   so.init(lane);
-  // next tile to transfer: index, head, row tile
+  // next tile to transfer: index, head, row tile; it goes to stage st, which
+  // callers pass as a constant (nx % kDkvStages)
   int nx = 0, nx_h = kvh * G, nx_rt = 0;
-  auto issue_next = [&]() {
-    const int st = nx % kDkvStages, r0 = rstart + nx_rt * kBR;
+  auto issue_next = [&](int st) __attribute__((always_inline)) {
+    const int r0 = rstart + nx_rt * kBR;
     const int64_t base = ((int64_t)r0 * a.hq + nx_h) * D;
     dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[st]);
     dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[st]);
@@ -218,17 +219,17 @@ dkv_kernel(BwdArgs a, int ktiles) {
   };
 
   // dS wave, one product stream per step: for the previous tile (stage sp,
-  // P buffer pbuf) dS = P o (dP - delta) in 16-row slices, each slice's
+  // also its P buffer) dS = P o (dP - delta) in 16-row slices, each slice's
   // dK^T[d][key] += Q^T[d][row] dS[row][key] products running beside the
   // elementwise work of the next slice; then (DP) dP[row][key] = dO V^T of
   // the current tile (stage st). The empty asm statements keep each slot's
   // vector work in its slot (IR passes would otherwise sink it to its use).
-  auto ds_dp = [&](int sp, int pbuf, int st, auto has_ds, auto has_dp) {
+  auto ds_dp = [&](int sp, int st, auto has_ds, auto has_dp) __attribute__((always_inline)) {
     constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
     constexpr int NK = DS ? NKK * NDB : 0, N = NK + (DP ? NKS * NRB : 0);
     const char *ql = (const char *)sm.q[sp];
     const char *dl = (const char *)sm.dout[st];
-    const u32x4 *pp = sm.p[pbuf][pair];
+    const u32x4 *pp = sm.p[sp][pair];
     u32x4 pw[NKK];
     f32x4 dlt[NRB][4];
     if constexpr (DS) {
@@ -242,7 +243,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
     }
     u32x4 fw[NKK];
     // dS elements 2u, 2u + 1 of slice kk (accumulator elements 8 bt + 2u ..)
-    auto ds_pair = [&](int kk, int u) {
+    auto ds_pair = [&](int kk, int u) __attribute__((always_inline)) {
       const int rb = kk >> 1, e0 = 8 * (kk & 1) + 2 * u;
       f32x2 x;
       x[0] = bf16_lo(pw[kk][u]) * (dp[rb][e0] - dlt[rb][e0 >> 2][e0 & 3]);
@@ -251,7 +252,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
       asm volatile("" : "+v"(w));
       fw[kk][u] = w;
     };
-    auto rd = [&](auto nc) -> bf16x8 {
+    auto rd = [&](auto nc) __attribute__((always_inline)) -> bf16x8 {
       constexpr int n = decltype(nc)::value;
       if constexpr (n < NK) {  // n = kk * NDB + db
         constexpr int kk = n / NDB, db = n % NDB;
@@ -261,7 +262,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         return *(const bf16x8 *)(dl + (j % NRB) * 32 * RB + so.row(j / NRB));
       }
     };
-    auto mm = [&](auto nc, bf16x8 x) {
+    auto mm = [&](auto nc, bf16x8 x) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       if constexpr (n < NK) {
         constexpr int kk = n / NDB, db = n % NDB;
@@ -271,17 +272,17 @@ dkv_kernel(BwdArgs a, int ktiles) {
         dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dp[rb]);
       }
     };
-    auto pre = [&](auto nc) {
+    auto pre = [&](auto nc) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       if constexpr (n == 2) {
-        if (nx < iters) issue_next();
+        if (nx < iters) issue_next((st + 1) % kDkvStages);
       }
       if constexpr (DS && n == 0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) ds_pair(0, u);
       }
     };
-    auto work = [&](auto nc) {
+    auto work = [&](auto nc) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       // slice kk + 1 during the NDB products of slice kk
       if constexpr (DS && n < NK - NDB) {
@@ -299,16 +300,16 @@ dkv_kernel(BwdArgs a, int ktiles) {
   // exponentials of block 1, then dV for block 1. P goes to LDS (and into
   // operand form) in 16-row slices; rows are masked unless every row sees
   // every key.
-  auto p_dv = [&](int st, int r0, int nvalid, int pbuf, bool full) {
+  auto p_dv = [&](int st, int r0, int nvalid, bool full) __attribute__((always_inline)) {
     const char *ql = (const char *)sm.q[st];
     const char *dl = (const char *)sm.dout[st];
-    u32x4 *pp = sm.p[pbuf][pair];
+    u32x4 *pp = sm.p[st][pair];
     f32x16 sacc[NRB];
     u32x4 fw[NKK];
     f32x4 l2[NRB][4];
     constexpr int NS = NKS * NRB;  // S products, row-block major
     constexpr int EPS = 16 / NKS;  // exponentials per slot
-    auto rd = [&](auto nc) -> bf16x8 {
+    auto rd = [&](auto nc) __attribute__((always_inline)) -> bf16x8 {
       constexpr int n = decltype(nc)::value;
       if constexpr (n < NS) {
         return *(const bf16x8 *)(ql + (n / NKS) * 32 * RB + so.row(n % NKS));
@@ -317,7 +318,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         return tr_operand_at(dl, 16 * kk * RB + so.tr(db, 0), 16 * kk * RB + so.tr(db, 1));
       }
     };
-    auto mm = [&](auto nc, bf16x8 x) {
+    auto mm = [&](auto nc, bf16x8 x) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       if constexpr (n < NS) {
         constexpr int rb = n / NKS, ks = n % NKS;
@@ -327,7 +328,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
       }
     };
-    auto mask_rb = [&](int rb) {
+    auto mask_rb = [&](int rb) __attribute__((always_inline)) {
       // rows at or past nvalid repeat the last row (clamped transfers)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -335,10 +336,10 @@ dkv_kernel(BwdArgs a, int ktiles) {
         if (rr >= nvalid || r0 + rr < seer_k) sacc[rb][r] = -INFINITY;
       }
     };
-    auto pre = [&](auto nc) {
+    auto pre = [&](auto nc) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       if constexpr (n == 2) {
-        if (nx < iters) issue_next();
+        if (nx < iters) issue_next((st + 1) % kDkvStages);
       }
       if constexpr (n == 0) {
 #pragma unroll
@@ -353,7 +354,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
     };
     // exponentials of block rb in the NKS slots after its S is complete;
     // each finished 16-row slice goes to LDS and operand form
-    auto work = [&](auto nc) {
+    auto work = [&](auto nc) __attribute__((always_inline)) {
       constexpr int n = decltype(nc)::value;
       if constexpr (n >= NKS && n < 3 * NKS) {
         constexpr int rb = n / NKS - 1, w = n % NKS;
@@ -380,11 +381,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
   for (int i = tid; i < (int)(sizeof(DkvSmem<D>) / 16); i += 512)
     ((u32x4 *)&sm)[i] = u32x4{};
   __syncthreads();
-  if (iters > 0) issue_next();
+  if (iters > 0) issue_next(0);
   // Start of step it (row tile rt): wait for its tile and synchronize; the
   // transfer of the next tile starts a few products into the step's product
   // stream (off the path to the first product). Returns the tile's first row.
-  auto begin_step = [&](int it, int &rt) {
+  auto begin_step = [&](int it, int &rt) __attribute__((always_inline)) {
     const int r0 = rstart + rt * kBR;
     if (++rt == nrt) rt = 0;
     wait_vmem();
@@ -395,36 +396,48 @@ dkv_kernel(BwdArgs a, int ktiles) {
     return r0;
   };
   // The two roles run separate loops (same barrier count) so that each
-  // keeps its accumulators in place.
+  // keeps its accumulators in place. Each loop is unrolled by the ring depth
+  // so that every tile, P and scalar buffer is a compile-time LDS offset.
+  static_assert(kDkvStages == 3, "the role loops below are unrolled by three");
   int rt = 0;
   if (pwave) {
-    for (int it = 0; it < iters; ++it) {
+    auto step = [&](int it, auto stc) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value;  // it % kDkvStages
       const int r0 = begin_step(it, rt);
       const int nvalid = min(kBR, e - r0);
       if (r0 + nvalid - 1 < seer_first) {  // no row sees these keys: P = 0
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) sm.p[it & 1][pair][kk * 64 + lane] = u32x4{};
-        if (nx < iters) issue_next();
-        continue;
+        for (int kk = 0; kk < NKK; ++kk) sm.p[st][pair][kk * 64 + lane] = u32x4{};
+        if (nx < iters) issue_next((st + 1) % kDkvStages);
+        return;
       }
-      p_dv(it % kDkvStages, r0, nvalid, it & 1, nvalid == kBR && r0 >= seer_last);
+      p_dv(st, r0, nvalid, nvalid == kBR && r0 >= seer_last);
+    };
+    for (int it = 0; it < iters; it += kDkvStages) {
+      step(it, std::integral_constant<int, 0>{});
+      if (it + 1 < iters) step(it + 1, std::integral_constant<int, 1>{});
+      if (it + 2 < iters) step(it + 2, std::integral_constant<int, 2>{});
     }
     lds_barrier();
   } else {
-    for (int it = 0; it < iters; ++it) {
+    // one stream per step: an invisible previous tile has P = 0 in LDS, so
+    // its dK products add nothing; an invisible current tile's dP is never
+    // used
+    auto step = [&](int it, auto stc) __attribute__((always_inline)) {
+      constexpr int st = decltype(stc)::value;  // it % kDkvStages
       const int r0 = begin_step(it, rt);
       const int nvalid = min(kBR, e - r0);
-      const bool vis = r0 + nvalid - 1 >= seer_first;
-      (void)vis;
-      // one stream per step: an invisible previous tile has P = 0 in LDS, so
-      // its dK products add nothing; an invisible current tile's dP is
-      // never used
-      ds_dp((it + kDkvStages - 1) % kDkvStages, (it - 1) & 1, it % kDkvStages, T_{}, T_{});
-      vis_prev = vis;
+      ds_dp((st + kDkvStages - 1) % kDkvStages, st, T_{}, T_{});
+      vis_prev = r0 + nvalid - 1 >= seer_first;
+    };
+    for (int it = 0; it < iters; it += kDkvStages) {
+      step(it, std::integral_constant<int, 0>{});
+      if (it + 1 < iters) step(it + 1, std::integral_constant<int, 1>{});
+      if (it + 2 < iters) step(it + 2, std::integral_constant<int, 2>{});
     }
     // finish the last tile once its P is in LDS
     lds_barrier();
-    if (vis_prev) ds_dp((iters - 1) % kDkvStages, (iters - 1) & 1, 0, T_{}, F_{});
+    if (vis_prev) ds_dp((iters - 1) % kDkvStages, 0, T_{}, F_{});
   }
 
   if (!wactive || key >= e) return;
