@@ -538,14 +538,16 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   __syncthreads();
 
   // keys past the row's bound get P = 0 (score -inf)
-  auto mask = [&](f32x16 &x, int k0) {
+  auto mask = [&](f32x16 &x, int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < 16; ++r)
       if (k0 + (r >> 2) * 8 + hf * 4 + (r & 3) > lim_r) x[r] = -INFINITY;
   };
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
+  // one key tile; the loop below runs it unrolled by two so that the buffer
+  // (t & 1) and with it every LDS address is a compile-time offset
+  auto step = [&](int t, auto bufc) __attribute__((always_inline)) {
+    constexpr int buf = decltype(bufc)::value;
     const int c0 = s + t * kBK;
     if (t + 1 < ntiles) {
       kt += tile_elems;
@@ -563,7 +565,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       constexpr int NH = 2 * NKS;  // products per half (S^T and dP^T)
       // products: [0, NH) S^T and dP^T half 0 (alternating), [NH, 2 NH) half 1,
       // [2 NH, 2 NH + 4 NDB) dQ^T (kb, db, bt)
-      auto rd = [&](auto nc) -> bf16x8 {
+      auto rd = [&](auto nc) __attribute__((always_inline)) -> bf16x8 {
         constexpr int n = decltype(nc)::value;
         if constexpr (n < 2 * NH) {
           constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
@@ -575,7 +577,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
           return tr_operand_at(kl, o + so.tr(db, 0), o + so.tr(db, 1));
         }
       };
-      auto mm = [&](auto nc, bf16x8 x) {
+      auto mm = [&](auto nc, bf16x8 x) __attribute__((always_inline)) {
         constexpr int n = decltype(nc)::value;
         if constexpr (n < 2 * NH) {
           constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
@@ -588,7 +590,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
         }
       };
       // mask a finished S^T half just before its exponentials start
-      auto pre = [&](auto nc) {
+      auto pre = [&](auto nc) __attribute__((always_inline)) {
         constexpr int n = decltype(nc)::value;
         if constexpr (n == NH) { if (!full) mask(sc[0], c0); }
         if constexpr (n == 2 * NH) { if (!full) mask(sc[1], c0 + 32); }
@@ -599,12 +601,12 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       // read them
       // (the empty asm keeps each result in its slot: IR passes would
       // otherwise sink the work past the mask branch to its uses)
-      auto exp1 = [&](int kb, int r) {
+      auto exp1 = [&](int kb, int r) __attribute__((always_inline)) {
         float p = fast_exp2(fmaf(sc[kb][r], sl2, -lse2));
         asm volatile("" : "+v"(p));
         sc[kb][r] = p;
       };
-      auto ds2 = [&](int kb, int r) {  // elements r, r + 1 (r even)
+      auto ds2 = [&](int kb, int r) __attribute__((always_inline)) {  // elements r, r + 1 (r even)
         f32x2 x;
         x[0] = sc[kb][r] * (pc[kb][r] - dlt);
         x[1] = sc[kb][r + 1] * (pc[kb][r + 1] - dlt);
@@ -612,7 +614,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
         asm volatile("" : "+v"(w));
         ds[kb][r >> 3][(r & 7) >> 1] = w;
       };
-      auto work = [&](auto nc) {
+      auto work = [&](auto nc) __attribute__((always_inline)) {
         constexpr int n = decltype(nc)::value;
         if constexpr (n >= NH && n < 2 * NH) {
           constexpr int E = 32 / NH, w = n - NH;  // element-steps per slot
@@ -638,6 +640,10 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
     }
     wait_vmem();
     __syncthreads();
+  };
+  for (int t = 0; t < ntiles; t += 2) {
+    step(t, std::integral_constant<int, 0>{});
+    if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
   }
 
   const int row = wq0 + l32;
