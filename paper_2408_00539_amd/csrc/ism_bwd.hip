@@ -157,11 +157,10 @@ dkv_kernel(BwdArgs a, int ktiles) {
 
   // (dialogue, KV head) groups run on one XCD each; early key tiles (the
   // longest row ranges) first.
-  const int total = a.batch * a.hkv * ktiles;
-  const int per = (total + 7) / 8;
-  const int item = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
-  if (item >= total) return;
-  const int group = item / ktiles, kt = item % ktiles;
+  int group, kt;
+  if (!xcd_work_item((int)blockIdx.x, a.batch * a.hkv, ktiles, ISM_SCHED_CHUNK, false, group,
+                     kt))
+    return;
   const int b = group / a.hkv, kvh = group % a.hkv;
   const int s = a.cu_seqlens[b], e = a.cu_seqlens[b + 1];
   const int c0 = s + kt * kKW;
@@ -176,25 +175,6 @@ dkv_kernel(BwdArgs a, int ktiles) {
   const int seer_last = (wactive && kw0 + 31 < e) ? a.seer[kw0 + 31] : e;
   const int key = kw0 + (lane & 31);
   const int seer_k = key < e ? a.seer[key] : 0x7fffffff;
-
-  // B operands of this wave's products: K (P wave, for S) or V (dS wave,
-  // for dP) of its 32 keys, lane <-> key, 8 head-dim values per k step
-  bf16x8 bop[NKS];
-  {
-    const int kr = min(key, e - 1);
-    const bf16_t *src =
-        (const bf16_t *)(pwave ? a.k : a.v) + ((int64_t)kr * a.hkv + kvh) * D + hf * 8;
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) bop[ks] = *(const bf16x8 *)(src + ks * 16);
-    wait_loads();
-  }
-  f32x16 acc[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
-  f32x16 dp[NRB];         // dS wave: dP of the previous tile
-#pragma unroll
-  for (int rb = 0; rb < NRB; ++rb) dp[rb] = f32x16{};
-  bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   const int rstart = a.seer[c0];
   const int nrt = (e - rstart + kBR - 1) / kBR;
@@ -217,6 +197,27 @@ dkv_kernel(BwdArgs a, int ktiles) {
     ++nx;
     if (++nx_rt == nrt) { nx_rt = 0; ++nx_h; }
   };
+  // B operands of this wave's products: K (P wave, for S) or V (dS wave,
+  // for dP) of its 32 keys, lane <-> key, 8 head-dim values per k step;
+  // the first tile's transfer overlaps their loads (iters >= 1: the first
+  // key's own row sees it).
+  bf16x8 bop[NKS];
+  {
+    const int kr = min(key, e - 1);
+    const bf16_t *src =
+        (const bf16_t *)(pwave ? a.k : a.v) + ((int64_t)kr * a.hkv + kvh) * D + hf * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) bop[ks] = *(const bf16x8 *)(src + ks * 16);
+    issue_next(0);
+    wait_loads();  // also drains the first transfer
+  }
+  f32x16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
+  f32x16 dp[NRB];         // dS wave: dP of the previous tile
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) dp[rb] = f32x16{};
+  bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   // dS wave, one product stream per step: for the previous tile (stage sp,
   // also its P buffer) dS = P o (dP - delta) in 16-row slices, each slice's
@@ -376,12 +377,19 @@ dkv_kernel(BwdArgs a, int ktiles) {
 
   using T_ = std::true_type;
   using F_ = std::false_type;
-  // Zero the LDS once: the dS waves' first step reads a P buffer, delta and
-  // Q stage that no tile has filled yet (and multiplies them by zeros).
-  for (int i = tid; i < (int)(sizeof(DkvSmem<D>) / 16); i += 512)
-    ((u32x4 *)&sm)[i] = u32x4{};
-  __syncthreads();
-  if (iters > 0) issue_next(0);
+  // The dS waves' first step reads the last stage's Q, P buffer and delta
+  // before any tile has filled them (and multiplies them by zeros): clear
+  // them. The first tile's transfer goes to stage 0 and is not touched.
+  {
+    constexpr int L = kDkvStages - 1;
+    u32x4 *qz = (u32x4 *)sm.q[L];
+    u32x4 *pz = (u32x4 *)sm.p[L];
+#pragma unroll
+    for (int i = tid; i < kBR * D / 8; i += 512) qz[i] = u32x4{};
+#pragma unroll
+    for (int i = tid; i < 4 * 4 * 64; i += 512) pz[i] = u32x4{};
+    if (tid < kBR) sm.delta[L][tid] = 0.f;
+  }
   // Start of step it (row tile rt): wait for its tile and synchronize; the
   // transfer of the next tile starts a few products into the step's product
   // stream (off the path to the first product). Returns the tile's first row.
@@ -422,7 +430,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
   } else {
     // one stream per step: an invisible previous tile has P = 0 in LDS, so
     // its dK products add nothing; an invisible current tile's dP is never
-    // used
+    // used. The first step's "previous tile" is the zeroed last stage.
     auto step = [&](int it, auto stc) __attribute__((always_inline)) {
       constexpr int st = decltype(stc)::value;  // it % kDkvStages
       const int r0 = begin_step(it, rt);
@@ -480,12 +488,10 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const int l32 = lane & 31, hf = lane >> 5;
 
   const int hsets = a.hq / hpw;
-  const int total = a.batch * hsets * tiles;
-  const int per = (total + 7) / 8;
-  const int item = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
-  if (item >= total) return;
-  const int group = item / tiles;
-  const int tile = tiles - 1 - item % tiles;
+  int group, tile;
+  if (!xcd_work_item((int)blockIdx.x, a.batch * hsets, tiles, ISM_SCHED_CHUNK, true, group,
+                     tile))
+    return;
   const int b = group / hsets;
   const int head0 = (group % hsets) * hpw;
   const int wg_rows = (4 / hpw) * 32;
@@ -501,6 +507,19 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const int wave_hi = active ? a.lim[min(wq0 + 32, e) - 1] : s - 1;
   const float sl2 = a.scale * kLog2e;
 
+  // The first K/V tile needs only the dialogue's key range in memory (keys
+  // past the workgroup's bound are masked like any other invisible key), so
+  // its transfer starts before the bounds, Q and dO arrive.
+  const bf16_t *kbase = (const bf16_t *)a.k + (int64_t)kvh * D;
+  const bf16_t *vbase = (const bf16_t *)a.v + (int64_t)kvh * D;
+  const int64_t rs = (int64_t)a.hkv * D;
+  DmaTile<D, kBK> dma;
+  dma.init(tid, rs);
+  const bf16_t *kt = kbase + (int64_t)s * rs;
+  const bf16_t *vt = vbase + (int64_t)s * rs;
+  dma.issue(kt, rs, e - s, sm.k[0]);
+  dma.issue(vt, rs, e - s, sm.v[0]);
+
   const int rc = min(wq0 + l32, e - 1);
   const int lim_r = a.lim[rc];
   const float lse2 = a.lse2[(int64_t)head * a.total + rc];
@@ -514,28 +533,18 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       qf[ks] = *(const bf16x8 *)(qp + ks * 16);
       df[ks] = *(const bf16x8 *)(dp + ks * 16);
     }
-    wait_loads();
+    wait_loads();  // also drains the transfers above
   }
+  __syncthreads();
   f32x16 dq[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) dq[db] = f32x16{};
 
-  const bf16_t *kbase = (const bf16_t *)a.k + (int64_t)kvh * D;
-  const bf16_t *vbase = (const bf16_t *)a.v + (int64_t)kvh * D;
-  const int64_t rs = (int64_t)a.hkv * D;
   const int ntiles = (key_hi - s) / kBK + 1;
   const int nw = active ? (wave_hi - s) / kBK + 1 : 0;  // this wave's tiles
-  DmaTile<D, kBK> dma;
-  dma.init(tid, rs);
   SwzBases<D> so;
   so.init(lane);
   const int64_t tile_elems = (int64_t)kBK * rs;
-  const bf16_t *kt = kbase + (int64_t)s * rs;
-  const bf16_t *vt = vbase + (int64_t)s * rs;
-  dma.issue(kt, rs, key_hi - s + 1, sm.k[0]);
-  dma.issue(vt, rs, key_hi - s + 1, sm.v[0]);
-  wait_vmem();
-  __syncthreads();
 
   // keys past the row's bound get P = 0 (score -inf)
   auto mask = [&](f32x16 &x, int k0) __attribute__((always_inline)) {
@@ -676,17 +685,16 @@ hipError_t launch_bwd_t(const BwdArgs &a, hipStream_t stream) {
   if (err != hipSuccess) return err;
 
   const int ktiles = (a.max_seqlen + kKW - 1) / kKW;
-  const int64_t tot_kv = (int64_t)a.batch * a.hkv * ktiles;
-  hipLaunchKernelGGL((dkv_kernel<D>), dim3((unsigned)(8 * ((tot_kv + 7) / 8))), dim3(512), 0,
-                     stream, a, ktiles);
+  hipLaunchKernelGGL((dkv_kernel<D>), dim3((unsigned)xcd_grid((int64_t)a.batch * a.hkv, ktiles)),
+                     dim3(512), 0, stream, a, ktiles);
   if ((err = hipGetLastError()) != hipSuccess) return err;
 
   const int hpw = gcd_i(a.hq / a.hkv, 4);
   const int wg_rows = (4 / hpw) * 32;
   const int tiles = (a.max_seqlen + wg_rows - 1) / wg_rows;
-  const int64_t tot_q = (int64_t)a.batch * (a.hq / hpw) * tiles;
-  hipLaunchKernelGGL((dq_kernel<D>), dim3((unsigned)(8 * ((tot_q + 7) / 8))), dim3(256), 0,
-                     stream, a, hpw, tiles);
+  hipLaunchKernelGGL((dq_kernel<D>),
+                     dim3((unsigned)xcd_grid((int64_t)a.batch * (a.hq / hpw), tiles)), dim3(256),
+                     0, stream, a, hpw, tiles);
   return hipGetLastError();
 }
 

@@ -292,6 +292,45 @@ __device__ __forceinline__ void product_slots(Rd &&rd, Mm &&mm, Pre &&pre, Work 
   product_slots_seq<N, LA>(rd, mm, pre, work, std::make_integer_sequence<int, N>{});
 }
 
+// Work order of (group, tile) items over the 8 XCDs. Consecutive workgroup
+// ids go to different XCDs (id % 8). With 8 or more groups, XCD x takes the
+// groups x, x + 8, x + 16, ... (so every XCD gets the same mix of dialogues)
+// and walks them in chunks of `chunk` groups; inside a chunk the tile index
+// runs over its groups innermost, in the order tiles-1 .. 0 (`high_first`,
+// row tiles of a causal-like mask, longest first) or 0 .. tiles-1 (key
+// tiles). The groups of one chunk keep their K/V (or Q/dO) in the XCD's L2
+// while their longest tiles start first, which also keeps the chip's last
+// workgroups short. With fewer than 8 groups every XCD takes every 8th item
+// of the same order over all groups. Returns false for ids past the end.
+#ifndef ISM_SCHED_CHUNK
+#define ISM_SCHED_CHUNK 4  // groups per scheduling chunk
+#endif
+__device__ __forceinline__ bool xcd_work_item(int bid, int groups, int tiles, int chunk,
+                                              bool high_first, int &group, int &tile) {
+  const int x = bid & 7, i = bid >> 3;
+  if (groups < 8) {
+    const int j = i * 8 + x;
+    if (j >= groups * tiles) return false;
+    tile = high_first ? tiles - 1 - j / groups : j / groups;
+    group = j % groups;
+    return true;
+  }
+  const int ng = (groups - x + 7) >> 3;  // groups of this XCD
+  if (i >= ng * tiles) return false;
+  const int ck = i / (chunk * tiles);
+  const int c0 = ck * chunk;
+  const int ce = min(chunk, ng - c0);
+  const int j = i - c0 * tiles;
+  tile = high_first ? tiles - 1 - j / ce : j / ce;
+  group = (c0 + j % ce) * 8 + x;
+  return true;
+}
+
+// Grid size for xcd_work_item: 8 x the largest per-XCD item count.
+inline int64_t xcd_grid(int64_t groups, int64_t tiles) {
+  return groups < 8 ? (groups * tiles + 7) / 8 * 8 : 8 * (((groups + 7) >> 3) * tiles);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) {
   return __builtin_bit_cast(float, w << 16);
 }

@@ -230,7 +230,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
 template <int D, bool CACHE>
 __global__ void __launch_bounds__(256)
 __attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
-fwd_kernel(FwdArgs a, int hpw, int tiles) {
+fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   constexpr int NDB = D / 32;      // 32-wide d blocks of the output
   constexpr int NKS = D / 16;      // 16-deep k steps of Q K^T
   __shared__ FwdSmem<D> sm;
@@ -239,16 +239,11 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int l32 = lane & 31, hf = lane >> 5;
 
-  // Work item: XCD-aware (consecutive workgroups land on different XCDs, so
-  // give each XCD a contiguous run of items), longest row tile first inside
-  // each (dialogue, head set) group.
+  // Work item: (dialogue, head set) groups in XCD-aware chunks, longest row
+  // tile first inside each chunk.
   const int hsets = a.hq / hpw;
-  const int total = a.batch * hsets * tiles;
-  const int per = (total + 7) / 8;
-  const int item = (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
-  if (item >= total) return;
-  const int group = item / tiles;
-  const int tile = tiles - 1 - item % tiles;
+  int group, tile;
+  if (!xcd_work_item((int)blockIdx.x, a.batch * hsets, tiles, chunk, true, group, tile)) return;
   const int b = group / hsets;
   const int head0 = (group % hsets) * hpw;
   const int wg_rows = (4 / hpw) * kQW;
@@ -286,6 +281,20 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
   // lazy rescale threshold: 2^8 in probability units
   const float tau = 8.f / sl2;
 
+  // Prologue, with its memory latencies overlapped: the transfers of K(0),
+  // V(0) and K(1) need only the dialogue's key range in memory (packed mode:
+  // keys past the workgroup's bound are real keys of the dialogue, masked
+  // like any other invisible key), so they start before the bounds and Q.
+  DmaTile<D, kBN> dma;
+  dma.init(tid, rs);
+  {
+    const int mem_rows = CACHE ? key_hi - key_begin + 1 : e - key_begin;
+    const bf16_t *k0 = kbase + (int64_t)key_begin * rs;
+    const bf16_t *v0 = vbase + (int64_t)key_begin * rs;
+    dma.issue(k0, rs, mem_rows, sm.k[0]);
+    dma.issue(v0, rs, mem_rows, sm.v[0]);
+    if (mem_rows > kBN) dma.issue(k0 + (int64_t)kBN * rs, rs, mem_rows - kBN, sm.k[1]);
+  }
   // Per-lane query row (clamped into the dialogue; rows past e are computed
   // as copies of the last row and never stored).
   const int rc = min(wq0 + l32, e - 1);
@@ -296,7 +305,8 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = *(const bf16x8 *)(qp + ks * 16);
   }
-  wait_loads();
+  wait_loads();  // Q, lim and the transfers above
+  __syncthreads();
 
   f32x16 oacc[NDB];
 #pragma unroll
@@ -313,18 +323,11 @@ fwd_kernel(FwdArgs a, int hpw, int tiles) {
   // are in flight into the other halves of the double buffers.
   const int ntiles = (key_hi - key_begin) / kBN + 1;  // for the workgroup
   const int nw = active ? (wave_hi - key_begin) / kBN + 1 : 0;  // this wave's
-  DmaTile<D, kBN> dma;
-  dma.init(tid, rs);
-  SwzOffsets<D> so;
-  so.init(lane);
   const int64_t tile_elems = (int64_t)kBN * rs;
   const bf16_t *kt = kbase + (int64_t)key_begin * rs;
   const bf16_t *vt = vbase + (int64_t)key_begin * rs;
-  dma.issue(kt, rs, key_hi - key_begin + 1, sm.k[0]);
-  dma.issue(vt, rs, key_hi - key_begin + 1, sm.v[0]);
-  if (ntiles > 1) dma.issue(kt + tile_elems, rs, key_hi - key_begin - kBN + 1, sm.k[1]);
-  wait_vmem();
-  __syncthreads();
+  SwzOffsets<D> so;
+  so.init(lane);
 
   f32x16 sa[2], sb[2];
   if (nw > 0) {
@@ -393,11 +396,10 @@ hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
   const int hpw = gcd_int(a.hq / a.hkv, 4);
   const int wg_rows = (4 / hpw) * kQW;
   const int tiles = (a.max_rows + wg_rows - 1) / wg_rows;
-  const int64_t total = (int64_t)a.batch * (a.hq / hpw) * tiles;
-  if (total == 0) return hipSuccess;
-  const int64_t per = (total + 7) / 8;
-  hipLaunchKernelGGL((fwd_kernel<D, CACHE>), dim3((unsigned)(8 * per)),
-                     dim3(256), 0, stream, a, hpw, tiles);
+  const int64_t groups = (int64_t)a.batch * (a.hq / hpw);
+  if (groups * tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((fwd_kernel<D, CACHE>), dim3((unsigned)xcd_grid(groups, tiles)),
+                     dim3(256), 0, stream, a, hpw, tiles, ISM_SCHED_CHUNK);
   return hipGetLastError();
 }
 
