@@ -1,7 +1,7 @@
 """Benchmark of the ISM attention hot path on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                [--only step|all] [--calibrate-copy]
+                [--only all|step|gqa|bwd|cache] [--calibrate-copy]
 
 A step is one training pass of the attention hot path over one batch of
 workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
@@ -11,6 +11,9 @@ and query head for the forward, 10*d for the backward. The other paths of the
 hot path are measured on their own workloads and reported under ``paths``:
 the grouped-KV forward (workload 2), the cached prefill and the decode stream
 (workload 3), the backward (workload 4).
+
+``--only gqa|bwd|cache`` measures that one path alone (for per-kernel
+profiles of one workload) and prints a JSON line with ``paths`` only.
 
 The last line of stdout is one JSON object; everything else goes to stderr.
 
@@ -271,7 +274,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["step", "all"], default="all")
+    ap.add_argument("--only", choices=["all", "step", "gqa", "bwd", "cache"],
+                    default="all")
     ap.add_argument("--calibrate-copy", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -291,6 +295,20 @@ def main():
         return
     timer = Timer()
     with_bwd = True
+    if args.only in ("gqa", "bwd", "cache"):
+        paths = {}
+        if args.only == "gqa":
+            w2 = W.make_workload(2)
+            t2 = bench_training(w2, timer, 10, 2, False)
+            paths["fwd_gqa"] = dict(t2["fwd"], workload="2x16384 h32/kv8 d128")
+        elif args.only == "bwd":
+            w4 = W.make_workload(4)
+            t4 = bench_training(w4, timer, 5, 1, True)
+            paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
+        else:
+            paths.update(bench_cache(W.make_workload(3), timer, 8, 2))
+        print(json.dumps({"paths": paths}), flush=True)
+        return
 
     log("generating workload 1 ...")
     w1 = W.make_workload(1)
