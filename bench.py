@@ -1,7 +1,8 @@
 """Benchmark of the ISM attention hot path on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                [--only all|step|gqa|bwd|cache] [--calibrate-copy]
+                [--only all|step|gqa|bwd|cache|expansion|latency]
+                [--calibrate-copy]
 
 A step is one training pass of the attention hot path over one batch of
 workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
@@ -12,8 +13,15 @@ hot path are measured on their own workloads and reported under ``paths``:
 the grouped-KV forward (workload 2), the cached prefill and the decode stream
 (workload 3), the backward (workload 4).
 
-``--only gqa|bwd|cache`` measures that one path alone (for per-kernel
-profiles of one workload) and prints a JSON line with ``paths`` only.
+Two comparisons from the paper ride along under ``paths``: the training cost
+of the prefix mask's sample expansion against ISM's single pass over the same
+dialogues (Sec. 1), and the per-turn latency experiment of Sec. 3.6 (ISM,
+causal and prefix masks; time to first token and per output token) at the
+level of one attention layer.
+
+``--only gqa|bwd|cache|expansion|latency`` measures that one path alone (for
+per-kernel profiles of one workload) and prints a JSON line with ``paths``
+only.
 
 The last line of stdout is one JSON object; everything else goes to stderr.
 
@@ -175,6 +183,113 @@ def bench_cache(w, timer, reps, warmup):
     return out
 
 
+def bench_expansion(w, timer, reps, warmup, ism_step_ms):
+    """Training on the dialogues of ``w`` the way a prefix-mask model must
+    (Sec. 1): every dialogue expanded into one sample per turn (history up to
+    Q_k as a bidirectional prefix, then A_k), one forward + backward over the
+    expanded batch; against ISM's single pass over the same dialogues."""
+    from paper_2408_00539_amd import ops, workloads as W
+    import torch
+    exp, src = W.prefix_expansion(w.segs)
+    segs = ops.Segments.from_host(exp.cu_seqlens, exp.cu_segs, exp.seg_is_query)
+    ix = torch.from_numpy(src).cuda()
+    q = dev(w.q).index_select(0, ix)
+    k = dev(w.k).index_select(0, ix)
+    v = dev(w.v).index_select(0, ix)
+    do = dev(w.do).index_select(0, ix)
+    pairs = visible_pairs(exp)
+    flop = 14 * w.d * w.hq * pairs
+
+    def step():
+        o, lse = ops.fwd(q, k, v, segs, w.scale)
+        ops.bwd(q, k, v, o, lse, do, segs, w.scale)
+    ms = timer.run(step, reps, warmup)
+    return {"train_prefix_expansion": {
+        "workload": "the dialogues of the training step, one sample per turn",
+        "samples": exp.batch, "tokens": exp.total, "ms": ms,
+        "tflops": flop / ms / 1e9, "flop": flop,
+        "ism_step_ms": ism_step_ms, "ism_speedup": ms / ism_step_ms}}
+
+
+LAT_B, LAT_TURNS, LAT_Q, LAT_A = 40, 20, 40, 160   # Sec. 3.6 latency workload
+LAT_HQ, LAT_HKV, LAT_D = 32, 8, 128
+
+
+def bench_latency(timer, reps=5, seed=5):
+    """The paper's latency experiment (Sec. 3.6: forty simulated dialogues of
+    20 turns, 40 query + 160 answer tokens per turn, context up to 4000) at
+    the level of one attention layer with 32 query / 8 KV heads, head_dim 128,
+    all forty dialogues batched. Per turn: time to first token = the new
+    query's prefill under ISM (query segment through the reused cache),
+    under the causal mask (the same rows causal) and under the prefix mask
+    (which cannot reuse the cache: the whole prefix is recomputed as one
+    bidirectional segment); time per output token = one decode step (the
+    same operation under all three masks: an answer token sees everything
+    before it). Inputs: seeded N(0, 1) bf16 drawn on the device."""
+    from paper_2408_00539_amd import ops
+    import torch
+    B, T_ctx = LAT_B, LAT_TURNS * (LAT_Q + LAT_A)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+
+    def rnd(*shape):
+        return torch.randn(*shape, generator=g, device="cuda",
+                           dtype=torch.float32).to(torch.bfloat16)
+    Q = rnd(B, T_ctx, LAT_HQ, LAT_D)
+    K = rnd(B, T_ctx, LAT_HKV, LAT_D)
+    V = rnd(B, T_ctx, LAT_HKV, LAT_D)
+    kc = torch.zeros(B, LAT_HKV, T_ctx, LAT_D, dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    cu_new = torch.arange(B + 1, dtype=torch.int32, device="cuda") * LAT_Q
+    ws = torch.empty(ops.workspace_size(ops.ISM_OP_DECODE, B, 0, T_ctx, LAT_HQ,
+                                        LAT_HKV, LAT_D, 0),
+                     dtype=torch.uint8, device="cuda")
+    scale = 1.0 / math.sqrt(LAT_D)
+    out = {m: [] for m in ("ttft_ism_ms", "ttft_causal_ms", "ttft_prefix_ms",
+                           "tpot_ms")}
+    for n in range(LAT_TURNS):
+        C = n * (LAT_Q + LAT_A)
+        P = C + LAT_Q
+        qn = Q[:, C:P].reshape(B * LAT_Q, LAT_HQ, LAT_D).contiguous()
+        kn = K[:, C:P].reshape(B * LAT_Q, LAT_HKV, LAT_D).contiguous()
+        vn = V[:, C:P].reshape(B * LAT_Q, LAT_HKV, LAT_D).contiguous()
+        clen = torch.full((B,), C, dtype=torch.int32, device="cuda")
+        for mode, isq in (("ttft_ism_ms", True), ("ttft_causal_ms", False)):
+            out[mode].append(timer.run(lambda: ops.prefill_cached_segment(
+                qn, kn, vn, kc, vc, clen, cu_new, LAT_Q, isq, scale), reps, 2))
+        # prefix mask: the whole prefix, one bidirectional segment per dialogue
+        cu = np.arange(B + 1, dtype=np.int32) * P
+        psegs = ops.Segments.from_host(cu, cu, np.ones(B, np.uint8))
+        qp = Q[:, :P].reshape(B * P, LAT_HQ, LAT_D).contiguous()
+        kp = K[:, :P].reshape(B * P, LAT_HKV, LAT_D).contiguous()
+        vp = V[:, :P].reshape(B * P, LAT_HKV, LAT_D).contiguous()
+        out["ttft_prefix_ms"].append(timer.run(
+            lambda: ops.fwd(qp, kp, vp, psegs, scale), reps, 2))
+        del qp, kp, vp
+        # the answer, one token per step
+        qd = Q[:, P:C + LAT_Q + LAT_A].transpose(0, 1).contiguous()
+        kd = K[:, P:C + LAT_Q + LAT_A].transpose(0, 1).contiguous()
+        vd = V[:, P:C + LAT_Q + LAT_A].transpose(0, 1).contiguous()
+        pos = (P + torch.arange(LAT_A, dtype=torch.int32, device="cuda"))[:, None]
+        pos = pos.expand(LAT_A, B).contiguous()
+
+        def answer():
+            for t in range(LAT_A):
+                ops.decode(qd[t], kd[t], vd[t], kc, vc, pos[t], T_ctx, scale,
+                           workspace=ws)
+        out["tpot_ms"].append(timer.run(answer, 1, 0) / LAT_A)
+    res = {"workload": f"{B} dialogues x {LAT_TURNS} turns x ({LAT_Q} query + "
+                       f"{LAT_A} answer) tokens, {LAT_HQ}/{LAT_HKV} heads, "
+                       f"head_dim {LAT_D}, one attention layer",
+           "turns_reported": [1, 5, 10, 15, 20]}
+    for m, vals in out.items():
+        res[m] = [round(vals[i - 1], 4) for i in res["turns_reported"]]
+        res[m.replace("_ms", "_mean_ms")] = round(float(np.mean(vals)), 4)
+    res["ttft_ism_minus_causal_us"] = round(
+        1000 * (res["ttft_ism_mean_ms"] - res["ttft_causal_mean_ms"]), 2)
+    return {"latency": res}
+
+
 def cpu_baseline(w, budget_s=15.0):
     """The fp64 oracle forward, as it stands, on a bounded sample of
     workload 1: the first n (dialogue, head) pairs, n chosen from a one-pair
@@ -274,7 +389,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", choices=["all", "step", "gqa", "bwd", "cache"],
+    ap.add_argument("--only", choices=["all", "step", "gqa", "bwd", "cache",
+                                       "expansion", "latency"],
                     default="all")
     ap.add_argument("--calibrate-copy", action="store_true")
     args = ap.parse_args()
@@ -295,7 +411,7 @@ def main():
         return
     timer = Timer()
     with_bwd = True
-    if args.only in ("gqa", "bwd", "cache"):
+    if args.only in ("gqa", "bwd", "cache", "expansion", "latency"):
         paths = {}
         if args.only == "gqa":
             w2 = W.make_workload(2)
@@ -305,8 +421,15 @@ def main():
             w4 = W.make_workload(4)
             t4 = bench_training(w4, timer, 5, 1, True)
             paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
-        else:
+        elif args.only == "cache":
             paths.update(bench_cache(W.make_workload(3), timer, 8, 2))
+        elif args.only == "expansion":
+            w1 = W.make_workload(1)
+            w1.do = W.packed_tensor(w1.seed, W.DO, w1.segs.cu_seqlens, w1.hq, w1.d)
+            tr = bench_training(w1, timer, 5, 1, True)
+            paths.update(bench_expansion(w1, timer, 3, 1, tr["step"]["ms"]))
+        else:
+            paths.update(bench_latency(timer))
         print(json.dumps({"paths": paths}), flush=True)
         return
 
@@ -340,6 +463,12 @@ def main():
         w3 = W.make_workload(3)
         paths.update(bench_cache(w3, timer, 8, 2))
         del w3
+        torch.cuda.empty_cache()
+        log("prefix-mask expansion of the step's dialogues ...")
+        paths.update(bench_expansion(w1, timer, 3, 1, step_ms))
+        torch.cuda.empty_cache()
+        log("latency turns ...")
+        paths.update(bench_latency(timer))
         torch.cuda.empty_cache()
 
     cpu = None

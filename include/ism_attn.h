@@ -123,6 +123,22 @@ ism_status ism_attn_prefill_cached(
     const int32_t *cache_seqlens, void *o, float *lse, int32_t hq, int32_t hkv,
     int32_t d, float scale, void *ws, size_t ws_bytes, void *stream);
 
+/* The same with the kind of the new segment given: seg_is_query != 0 is the
+ * query segment of ism_attn_prefill_cached; seg_is_query == 0 appends an
+ * answer segment, whose row r (0-based inside the segment) sees keys
+ * [0, C_b + r] (Eq. 5 third case, f(j) = j): an answer prefilled in chunks
+ * through the cache, or the causal mask of Eq. 2 for the new rows (the
+ * baseline the paper's latency comparison measures ISM against, Sec. 3.6).
+ * All other arguments, the append and the errors are as for
+ * ism_attn_prefill_cached. */
+ism_status ism_attn_prefill_cached_segment(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
+    int32_t max_new, int32_t seg_is_query, const void *q_new,
+    const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+    int32_t cache_cap, const int32_t *cache_seqlens, void *o, float *lse,
+    int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+    size_t ws_bytes, void *stream);
+
 /* One answer-token decode step with the reused cache (Sec. 2.3, generation
  * of A_n; Eq. 5 third case f(j) = j: the new token sees every cached token
  * and itself). For dialogue b the new token sits at position

@@ -286,13 +286,17 @@ def bwd(q, k, v, do, cu_seqlens, cu_segs, seg_is_query, scale, pairs=None,
 # Inference with KV-cache reuse (Sec. 2.3)
 # --------------------------------------------------------------------------
 
-def prefill_cached(k_hist, v_hist, q_new, k_new, v_new, scale):
-    """One dialogue's new query segment Q_n against the cached history C_h.
+def prefill_cached(k_hist, v_hist, q_new, k_new, v_new, scale,
+                   new_is_query=True):
+    """One dialogue's new segment against the cached history C_h.
 
     Sec. 2.3: reuse C_h, compute C_q from the new tokens, concatenate
-    [C_h; C_q]. By Eq. 5 (f = m_{q_n} for every token of Q_n) each new row
-    sees every key of the concatenation. Shapes: k_hist/v_hist [C, Hkv, d],
-    q_new [L, Hq, d], k_new/v_new [L, Hkv, d]. Returns
+    [C_h; C_q]. For a query segment Q_n (Eq. 5 first two cases, f = m_{q_n}
+    for every token of Q_n) each new row sees every key of the concatenation.
+    For an answer segment (``new_is_query=False``; Eq. 5 third case,
+    f(j) = j) new row r sees the history and the new rows 0..r: the causal
+    mask of Eq. 2 restricted to these rows. Shapes: k_hist/v_hist
+    [C, Hkv, d], q_new [L, Hq, d], k_new/v_new [L, Hkv, d]. Returns
     (o [L, Hq, d], lse [Hq, L], k_cat, v_cat).
     """
     k_cat = np.concatenate([k_hist, k_new], axis=0).astype(np.float64)
@@ -301,7 +305,11 @@ def prefill_cached(k_hist, v_hist, q_new, k_new, v_new, scale):
     G = _group(hq, k_cat.shape[1])
     o = np.empty((L, hq, d))
     lse = np.empty((hq, L))
-    vis = np.ones((L, k_cat.shape[0]), dtype=bool)
+    C = k_hist.shape[0]
+    if new_is_query:
+        vis = np.ones((L, C + L), dtype=bool)
+    else:
+        vis = np.arange(C + L)[None, :] <= C + np.arange(L)[:, None]
     for h in range(hq):
         qh = np.asarray(q_new[:, h], dtype=np.float64)
         o[:, h], lse[h] = _softmax_attend(qh, k_cat[:, h // G],

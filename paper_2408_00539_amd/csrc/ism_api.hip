@@ -202,6 +202,18 @@ extern "C" ism_status ism_attn_prefill_cached(
     void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens, void *o,
     float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
     size_t ws_bytes, void *stream) {
+  return ism_attn_prefill_cached_segment(cu_seqlens_new, batch, total_new, max_new, 1,
+                                         q_new, k_new, v_new, k_cache, v_cache, cache_cap,
+                                         cache_seqlens, o, lse, hq, hkv, d, scale, ws,
+                                         ws_bytes, stream);
+}
+
+extern "C" ism_status ism_attn_prefill_cached_segment(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
+    int32_t seg_is_query, const void *q_new, const void *k_new, const void *v_new,
+    void *k_cache, void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens, void *o,
+    float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+    size_t ws_bytes, void *stream) {
   ism::clear_error();
   if (!cu_seqlens_new || !q_new || !k_new || !v_new || !k_cache || !v_cache ||
       !cache_seqlens || !o)
@@ -235,6 +247,7 @@ extern "C" ism_status ism_attn_prefill_cached(
   a.kv_head_stride = (int64_t)cache_cap * d;
   a.kv_row_stride = d;
   a.scale = scale;
+  a.cache_causal = seg_is_query ? 0 : 1;
   return hip_status(ism::launch_fwd(a, d, true, s), "cached prefill launch");
 }
 

@@ -257,14 +257,23 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   const bool active = wq0 < e;
   const int wg_last = min(q0 + wg_rows, e) - 1;
 
-  int key_begin, key_hi, wave_lo, wave_hi;
+  int key_begin, key_hi, wave_lo, wave_hi, cache_c = 0;
   const bf16_t *kbase, *vbase;
   if (CACHE) {
     key_begin = 0;
-    // keys [0, C_b + L_b); clamped to the slab for out-of-contract lengths
-    key_hi = max(min(a.cache_len[b] + (e - s), a.kv_head_stride / D) - 1, 0);
-    wave_lo = key_hi;
-    wave_hi = active ? key_hi : -1;
+    cache_c = a.cache_len[b];
+    // keys [0, C_b + L_b) (query segment) or [0, C_b + r] for row r (answer
+    // segment); clamped to the slab for out-of-contract lengths
+    const int slab_rows = (int)(a.kv_head_stride / D);
+    if (a.cache_causal) {
+      key_hi = max(min(cache_c + (wg_last - s) + 1, slab_rows) - 1, 0);
+      wave_lo = min(cache_c + (min(wq0, e - 1) - s), key_hi);
+      wave_hi = active ? min(cache_c + (min(wq0 + kQW, e) - 1 - s), key_hi) : -1;
+    } else {
+      key_hi = max(min(cache_c + (e - s), slab_rows) - 1, 0);
+      wave_lo = key_hi;
+      wave_hi = active ? key_hi : -1;
+    }
     const int64_t off = (int64_t)b * a.kv_seq_stride + (int64_t)kvh * a.kv_head_stride;
     kbase = (const bf16_t *)a.k + off;
     vbase = (const bf16_t *)a.v + off;
@@ -298,7 +307,9 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   // Per-lane query row (clamped into the dialogue; rows past e are computed
   // as copies of the last row and never stored).
   const int rc = min(wq0 + l32, e - 1);
-  const int lim_r = CACHE ? key_hi : a.lim[rc];
+  const int lim_r = !CACHE          ? a.lim[rc]
+                    : a.cache_causal ? min(cache_c + (rc - s), key_hi)
+                                     : key_hi;
   bf16x8 qf[NKS];
   {
     const bf16_t *qp = (const bf16_t *)a.q + ((int64_t)rc * a.hq + head) * D + hf * 8;

@@ -10,8 +10,9 @@ namespace ism {
 //  * packed (training / prefill): rows and keys live on the packed token axis,
 //    key i of dialogue b is row i of k/v (stride hkv*d), and row j sees keys
 //    [cu_q[b], lim[j]];
-//  * cache (KV reuse): rows are the new query tokens of dialogue b, keys are
-//    rows 0..C_b+L_b-1 of that dialogue's cache slab, all visible.
+//  * cache (KV reuse): rows are the new tokens of dialogue b, keys are rows
+//    of that dialogue's cache slab: all of 0..C_b+L_b-1 for a new query
+//    segment, 0..C_b+r for row r of a new answer segment (cache_causal).
 struct FwdArgs {
   const void *q;
   const void *k;
@@ -30,6 +31,8 @@ struct FwdArgs {
   int64_t kv_head_stride;   // elements between KV heads
   int64_t kv_row_stride;    // elements between consecutive keys
   float scale;
+  int32_t cache_causal;     // cache mode: the new segment is an answer
+                            // segment (row r sees keys [0, C_b + r])
 };
 
 hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,

@@ -7,7 +7,7 @@ fallback: if the library is not built or no gfx950 device is present, the
 call fails loudly.
 
 Names follow the C ABI (include/ism_attn.h): fwd, bwd, prefill_cached,
-decode, plus check_segments_host and workspace_size.
+prefill_cached_segment, decode, plus check_segments_host and workspace_size.
 """
 
 from __future__ import annotations
@@ -55,6 +55,9 @@ _SIGS = {
                           _P, _P, _P, _P, _I, _I, _I, _F, _I, _P, _Z, _P]),
     "ism_attn_prefill_cached": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P, _I,
                                      _P, _P, _P, _I, _I, _I, _F, _P, _Z, _P]),
+    "ism_attn_prefill_cached_segment": (_I, [_P, _I, _I, _I, _I, _P, _P, _P,
+                                             _P, _P, _I, _P, _P, _P, _I, _I,
+                                             _I, _F, _P, _Z, _P]),
     "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
                              _I, _I, _F, _I, _P, _Z, _P]),
     "ism_check_segments_host": (_I, [_P, _P, _P, _I, _I, _I, _I]),
@@ -217,6 +220,23 @@ def prefill_cached(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
                    cu_seqlens_new, max_new, scale=None, return_lse=True):
     """New query segment against the reused cache (appends k_new/v_new).
     Returns (o [Tn,hq,d] bf16, lse [hq,Tn] fp32 or None)."""
+    return _prefill(None, q_new, k_new, v_new, k_cache, v_cache,
+                    cache_seqlens, cu_seqlens_new, max_new, scale, return_lse)
+
+
+def prefill_cached_segment(q_new, k_new, v_new, k_cache, v_cache,
+                           cache_seqlens, cu_seqlens_new, max_new,
+                           seg_is_query, scale=None, return_lse=True):
+    """New segment against the reused cache: a query segment (every new row
+    sees the whole cache and all new rows) or, with seg_is_query false, an
+    answer segment (new row r sees the cache and new rows 0..r)."""
+    return _prefill(bool(seg_is_query), q_new, k_new, v_new, k_cache,
+                    v_cache, cache_seqlens, cu_seqlens_new, max_new, scale,
+                    return_lse)
+
+
+def _prefill(seg_is_query, q_new, k_new, v_new, k_cache, v_cache,
+             cache_seqlens, cu_seqlens_new, max_new, scale, return_lse):
     torch = _torch()
     Tn, hq, d = q_new.shape
     B, hkv, cap, _ = k_cache.shape
@@ -231,10 +251,18 @@ def prefill_cached(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
     o = torch.empty_like(q_new)
     lse = torch.empty((hq, Tn), dtype=torch.float32, device=q_new.device) \
         if return_lse else None
-    _check(lib().ism_attn_prefill_cached(
-        _ptr(cu_seqlens_new), B, Tn, int(max_new), _ptr(q_new), _ptr(k_new),
-        _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap, _ptr(cache_seqlens),
-        _ptr(o), _ptr(lse), hq, hkv, d, scale, None, 0, _stream()))
+    if seg_is_query is None:
+        _check(lib().ism_attn_prefill_cached(
+            _ptr(cu_seqlens_new), B, Tn, int(max_new), _ptr(q_new),
+            _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap,
+            _ptr(cache_seqlens), _ptr(o), _ptr(lse), hq, hkv, d, scale, None,
+            0, _stream()))
+    else:
+        _check(lib().ism_attn_prefill_cached_segment(
+            _ptr(cu_seqlens_new), B, Tn, int(max_new), int(seg_is_query),
+            _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
+            _ptr(v_cache), cap, _ptr(cache_seqlens), _ptr(o), _ptr(lse), hq,
+            hkv, d, scale, None, 0, _stream()))
     return o, lse
 
 

@@ -172,6 +172,42 @@ def alternating(lengths, first_is_query=True):
             for i, n in enumerate(lengths)]
 
 
+def prefix_expansion(segs):
+    """The multi-sample layout a prefix-mask model trains on (Sec. 1): every
+    dialogue [Q_1, A_1, ..., Q_n, A_n] becomes n samples, sample k being the
+    history up to Q_k as one bidirectional prefix (Eq. 3) followed by A_k as
+    a causal answer. ISM covers the same answers in one pass over the
+    dialogue.
+
+    Returns (expanded Segments, src) where src[t] is the token of the
+    original packed axis that expanded token t copies (so expanded tensors
+    are gathers of the original ones). Dialogues must alternate query /
+    answer segments starting with a query; a trailing query segment without
+    an answer yields no sample.
+    """
+    cu, cs, fl = segs.cu_seqlens, segs.cu_segs, segs.seg_is_query
+    samples, src = [], []
+    g = 0
+    for b in range(segs.batch):
+        s, e = int(cu[b]), int(cu[b + 1])
+        while g < len(fl) and cs[g] < e:
+            a, c = int(cs[g]), int(cs[g + 1])
+            if not fl[g]:
+                raise ValueError("dialogues must alternate query / answer "
+                                 "segments starting with a query")
+            if g + 1 < len(fl) and cs[g + 1] < e:
+                if fl[g + 1]:
+                    raise ValueError("two adjacent query segments")
+                a2 = int(cs[g + 2])
+                samples.append([(c - s, True), (a2 - c, False)])
+                src.append(np.arange(s, a2, dtype=np.int64))
+                g += 2
+            else:
+                g += 1
+    exp = segments_from_lengths(samples)
+    return exp, (np.concatenate(src) if src else np.zeros(0, np.int64))
+
+
 # --------------------------------------------------------------------------
 # Tensors
 # --------------------------------------------------------------------------

@@ -135,6 +135,14 @@ def test_cache_argument_errors(L):
     assert L.ism_attn_prefill_cached(FAKE, 1, 10, 10, FAKE, FAKE, FAKE, None,
                                      FAKE, 64, FAKE, FAKE, None, 1, 1, 64, 0.125,
                                      None, 0, None) == 1
+    # prefill of an answer segment: the same checks
+    for flag in (0, 1):
+        assert L.ism_attn_prefill_cached_segment(
+            FAKE, 1, 10, 10, flag, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE, FAKE,
+            None, 1, 1, 64, 0.125, None, 0, None) == 6
+        assert L.ism_attn_prefill_cached_segment(
+            FAKE, 1, 10, 10, flag, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE,
+            None, None, 1, 1, 64, 0.125, None, 0, None) == 1
     # bwd: null gradient output
     sg = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
     assert L.ism_attn_bwd(ctypes.byref(sg), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,

@@ -91,6 +91,39 @@ def test_prefill_then_decode_small(d, hq, hkv):
         pos += 1
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (8, 2)])
+def test_prefill_answer_segment_small(d, hq, hkv):
+    """ism_attn_prefill_cached_segment with an answer segment (Eq. 5 third
+    case: new row r sees the cache and new rows 0..r) against the oracle;
+    the query form of the same entry point against the query oracle."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    rng = np.random.default_rng(7 * d + hq)
+    hist = [0, 1, 64, 65, 300, 127]
+    new = [1, 64, 130, 65, 200, 33]
+    cap = 640
+    scale = 1 / np.sqrt(d)
+    for isq in (False, True):
+        kc, vc, cu_new, qn, kn, vn = _setup(rng, hist, new, hq, hkv, d, cap)
+        announce("prefill segment", "query" if isq else "answer", d, hq, hkv)
+        o, lse = ops.prefill_cached_segment(
+            dev_bf16(qn), dev_bf16(kn), dev_bf16(vn), dev_bf16(kc), dev_bf16(vc),
+            torch.tensor(hist, dtype=torch.int32, device="cuda"),
+            torch.from_numpy(cu_new).cuda(), max(new), isq, scale)
+        torch.cuda.synchronize()
+        o, lse = host_f64(o), host_f64(lse)
+        for b, C in enumerate(hist):
+            r0, r1 = cu_new[b], cu_new[b + 1]
+            ro, rl, _, _ = oracle.prefill_cached(
+                f64(kc[b, :, :C]).transpose(1, 0, 2),
+                f64(vc[b, :, :C]).transpose(1, 0, 2),
+                f64(qn[r0:r1]), f64(kn[r0:r1]), f64(vn[r0:r1]), scale,
+                new_is_query=isq)
+            compare(f"O b{b} q={isq}", o[r0:r1], ro)
+            compare(f"LSE b{b} q={isq}", lse[:, r0:r1], rl)
+
+
 def test_decode_split_counts_agree():
     """Any split count merges to the same result (exact merge, R19)."""
     torch = torch_cuda()

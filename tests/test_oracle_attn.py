@@ -202,6 +202,36 @@ def test_stepwise_cache_equals_one_shot(hq, hkv):
     assert kc.shape[0] == T
 
 
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_cached_answer_segment_equals_one_shot(hq, hkv):
+    """Sec. 2.3 with an answer segment appended through the cache (Eq. 5
+    third case): its rows equal the one-shot forward over [history; A] with A
+    an answer segment, and equal the answer rows produced one token at a
+    time by decode steps."""
+    rng = np.random.default_rng(9)
+    hist = [4, 6, 3]                 # Q A Q
+    La, d = 7, 8
+    segs = segments_from_lengths([alternating(hist + [La])])
+    T = segs.total
+    q, k, v = _rand(rng, T, hq, d), _rand(rng, T, hkv, d), _rand(rng, T, hkv, d)
+    o, lse = _fwd(q, k, v, segs, 0.5)
+    C = sum(hist)
+    on, ln_, _, _ = oracle.prefill_cached(k[:C], v[:C], q[C:], k[C:], v[C:],
+                                          0.5, new_is_query=False)
+    np.testing.assert_allclose(on, o[C:], atol=1e-12)
+    np.testing.assert_allclose(ln_, lse[:, C:], atol=1e-12)
+    kc, vc = k[:C], v[:C]
+    for t in range(La):
+        ot, lt, kc, vc = oracle.decode_step(kc, vc, q[C + t], k[C + t],
+                                            v[C + t], 0.5)
+        np.testing.assert_allclose(ot, on[t], atol=1e-12)
+        np.testing.assert_allclose(lt, ln_[:, t], atol=1e-12)
+    # the query form of the same rows differs (every row sees all of A)
+    oq, _, _, _ = oracle.prefill_cached(k[:C], v[:C], q[C:], k[C:], v[C:], 0.5)
+    assert np.max(np.abs(oq[:-1] - on[:-1])) > 1e-3
+    np.testing.assert_allclose(oq[-1], on[-1], atol=1e-12)
+
+
 # ------------------------------------------------------ P-11..P-13 backward
 
 def _loss_setup(seed, hq, hkv, d):
