@@ -86,8 +86,10 @@ ism_status hip_status(hipError_t e, const char *what) {
 
 int decode_splits(int32_t batch, int32_t hkv, int32_t max_len, int32_t req) {
   if (req > 0) return req;
+  // about 2048 workgroups (two rounds of four per CU), at least 256 keys
+  // per chunk, at most 64 chunks
   const int slabs = batch * hkv;
-  int s = (4096 + slabs - 1) / slabs;
+  int s = (2048 + slabs - 1) / slabs;
   const int by_len = (max_len + 255) / 256;
   if (s > by_len) s = by_len;
   if (s > 64) s = 64;

@@ -63,8 +63,9 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
   const int64_t pairs = (int64_t)total * hq;
   const int64_t rh = min(gid / LPR, pairs - 1);
   const int c = (int)(gid % LPR);
-  const u32x4 x = *(const u32x4 *)(o + rh * D + c * 8);
-  const u32x4 y = *(const u32x4 *)(dout + rh * D + c * 8);
+  // read once: non-temporal loads keep them out of the caches
+  const u32x4 x = __builtin_nontemporal_load((const u32x4 *)(o + rh * D + c * 8));
+  const u32x4 y = __builtin_nontemporal_load((const u32x4 *)(dout + rh * D + c * 8));
   float acc = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
