@@ -167,8 +167,9 @@ __device__ __forceinline__ void tile_pv(const char *vl, const SwzOffsets<D> &so,
 // during the P V products the row max of S(t+1). The order is pinned with
 // scheduling barriers so that the matrix core and the vector ALU of a wave
 // are busy at the same time. Returns the fp32 row sum of P(t); mt receives
-// the (unmasked) row max of S(t+1).
-template <int D>
+// the (unmasked) row max of S(t+1). With LAST (a wave's last tile) there is
+// no S(t+1): the exponentials run alone, then the P V products.
+template <int D, bool LAST>
 __device__ __forceinline__ float step_block(const char *kl, const char *vl,
                                             const SwzOffsets<D> &so, const bf16x8 (&qf)[D / 16],
                                             const f32x16 (&cur)[2], f32x16 (&nxt)[2],
@@ -187,21 +188,24 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
     const uint32_t o = ((kc >> 1) * 32 + 16 * (kc & 1)) * D * 2;
     return tr_operand_at(vl, o + so.trk[db][0], o + so.trk[db][1]);
   };
+  constexpr int F = LAST ? NS : 0;  // first product that runs
   bf16x8 op[N];
 #pragma unroll
-  for (int n = 0; n < LA; ++n) op[n] = read(n);
+  for (int n = F; n < F + LA; ++n) op[n] = read(n);
   u32x4 w[2][2];
   float sum[2] = {0.f, 0.f}, mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
   for (int n = 0; n < N; ++n) {
     if (n < NS) {
-      const int kb = n / NKS, ks = n % NKS;
-      nxt[kb] = mfma32x32x16(op[n], qf[ks], ks == 0 ? f32x16{} : nxt[kb]);
+      if (!LAST) {
+        const int kb = n / NKS, ks = n % NKS;
+        nxt[kb] = mfma32x32x16(op[n], qf[ks], ks == 0 ? f32x16{} : nxt[kb]);
+      }
     } else {
       const int j = n - NS, kc = j / NDB, db = j % NDB;
       oacc[db] = mfma32x32x16(op[n], __builtin_bit_cast(bf16x8, w[kc >> 1][kc & 1]), oacc[db]);
     }
-    if (n + LA < N) op[n + LA] = read(n + LA);
+    if (n >= F && n + LA < N) op[n + LA] = read(n + LA);
     if (n < NS) {
 #pragma unroll
       for (int c = 0; c < PPS; ++c) {
@@ -213,7 +217,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
         w[kb][bt][u] = cvt_bf16x2(p);
         asm volatile("" : "+v"(sum[i & 1]));  // keep the add in this slot
       }
-    } else {
+    } else if (!LAST) {
 #pragma unroll
       for (int c = 0; c < MPP; c += 2) {
         const int e = (n - NS) * MPP + c, m = (e >> 1) & 1;
@@ -223,7 +227,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-  mt = pair_max(vmax(mx[0], mx[1]));
+  mt = LAST ? -INFINITY : pair_max(vmax(mx[0], mx[1]));
   return sum[0] + sum[1];
 }
 
@@ -348,22 +352,26 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   }
   lds_barrier();  // every wave is done with K(0) before K(2) overwrites it
 
-  auto step = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], int t) {
+  // Step t; LAST is the workgroup's last tile, which has no S(t+1): the
+  // waves whose last tile it is run the exponentials and P V only. (A wave
+  // whose last tile comes earlier computes an unused S(t+1) there, which
+  // keeps one code path inside the loop.)
+  auto step = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], int t, auto lastc) {
+    constexpr bool LAST = decltype(lastc)::value;
     const int c0 = key_begin + t * kBN;
-    if (t + 2 < ntiles)
-      dma.issue(kt + 2 * tile_elems, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
-    if (t + 1 < ntiles)
+    if (!LAST) {
+      if (t + 2 < ntiles)
+        dma.issue(kt + 2 * tile_elems, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
       dma.issue(vt + tile_elems, rs, key_hi - (c0 + kBN) + 1, sm.v[(t + 1) & 1]);
-    kt += tile_elems;
-    vt += tile_elems;
+      kt += tile_elems;
+      vt += tile_elems;
+    }
     const char *kl = (const char *)sm.k[(t + 1) & 1];
     const char *vl = (const char *)sm.v[t & 1];
     if (t < nw) {
-      // the last tile of a wave also computes an (unused) S(t+1) from
-      // whatever the K buffer holds, which keeps one code path per step
       float mt;
-      l_run += step_block<D>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt);
-      if (t + 1 < nw) {
+      l_run += step_block<D, LAST>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt);
+      if (!LAST && t + 1 < nw) {
         if (c0 + 2 * kBN - 1 > wave_lo) {  // S(t+1) crosses some row's bound
           tile_mask(nxt, c0 + kBN, hf, lim_r);
           mt = tile_max(nxt);
@@ -374,10 +382,13 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     wait_vmem();
     __syncthreads();
   };
-  for (int t = 0; t < ntiles; t += 2) {
-    step(sa, sb, t);
-    if (t + 1 < ntiles) step(sb, sa, t + 1);
+  const std::false_type mid{};
+  for (int t = 0; t + 1 < ntiles; t += 2) {
+    step(sa, sb, t, mid);
+    if (t + 2 < ntiles) step(sb, sa, t + 1, mid);
   }
+  if ((ntiles - 1) & 1) step(sb, sa, ntiles - 1, std::true_type{});
+  else step(sa, sb, ntiles - 1, std::true_type{});
 
   if (!active) return;
   const float lt = pair_sum(l_run);
