@@ -3,11 +3,11 @@
 // accumulation. The same kernel serves the cached prefill of a new query
 // segment (Sec. 2.3), where every key of the concatenated cache is visible.
 //
-// Work decomposition. A workgroup (4 waves) owns a row tile of one dialogue
-// and a set of query heads that share one KV head: with G = hq / hkv query
-// heads per KV head, hpw = gcd(G, 4) heads run side by side (one per wave
-// column) so that the K/V tile staged in LDS serves all of them, and the
-// remaining 4 / hpw waves take consecutive 32-row blocks. Each wave
+// Work decomposition. A workgroup (NWV = 4 or 8 waves) owns a row tile of one
+// dialogue and a set of query heads that share one KV head: with G = hq / hkv
+// query heads per KV head, hpw = gcd(G, NWV) heads run side by side (one per
+// wave column) so that the K/V tile staged in LDS serves all of them, and the
+// remaining NWV / hpw waves take consecutive 32-row blocks. Each wave
 // computes S^T = K Q^T for a 64-key tile (lane <-> query row, so the softmax
 // statistics of a row live in one lane pair), then O^T += V^T P^T.
 //
@@ -231,8 +231,8 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
   return sum[0] + sum[1];
 }
 
-template <int D, bool CACHE>
-__global__ void __launch_bounds__(256)
+template <int D, bool CACHE, int NWV>
+__global__ void __launch_bounds__(NWV * 64)
 __attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
 fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   constexpr int NDB = D / 32;      // 32-wide d blocks of the output
@@ -250,7 +250,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   if (!xcd_work_item((int)blockIdx.x, a.batch * hsets, tiles, chunk, true, group, tile)) return;
   const int b = group / hsets;
   const int head0 = (group % hsets) * hpw;
-  const int wg_rows = (4 / hpw) * kQW;
+  const int wg_rows = (NWV / hpw) * kQW;
   const int s = a.cu_q[b], e = a.cu_q[b + 1];
   const int q0 = s + tile * wg_rows;
   if (q0 >= e) return;
@@ -298,7 +298,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   // V(0) and K(1) need only the dialogue's key range in memory (packed mode:
   // keys past the workgroup's bound are real keys of the dialogue, masked
   // like any other invisible key), so they start before the bounds and Q.
-  DmaTile<D, kBN> dma;
+  DmaTile<D, kBN, NWV> dma;
   dma.init(tid, rs);
   {
     const int mem_rows = CACHE ? key_hi - key_begin + 1 : e - key_begin;
@@ -413,16 +413,27 @@ int gcd_int(int x, int y) {
   return x;
 }
 
-template <int D, bool CACHE>
-hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
-  const int hpw = gcd_int(a.hq / a.hkv, 4);
-  const int wg_rows = (4 / hpw) * kQW;
+template <int D, bool CACHE, int NWV>
+hipError_t launch_fwd_w(const FwdArgs &a, hipStream_t stream) {
+  const int hpw = gcd_int(a.hq / a.hkv, NWV);
+  const int wg_rows = (NWV / hpw) * kQW;
   const int tiles = (a.max_rows + wg_rows - 1) / wg_rows;
   const int64_t groups = (int64_t)a.batch * (a.hq / hpw);
   if (groups * tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((fwd_kernel<D, CACHE>), dim3((unsigned)xcd_grid(groups, tiles)),
-                     dim3(256), 0, stream, a, hpw, tiles, ISM_SCHED_CHUNK);
+  hipLaunchKernelGGL((fwd_kernel<D, CACHE, NWV>), dim3((unsigned)xcd_grid(groups, tiles)),
+                     dim3(NWV * 64), 0, stream, a, hpw, tiles, ISM_SCHED_CHUNK);
   return hipGetLastError();
+}
+
+// Grouped KV heads run 8-wave workgroups (one per CU): the heads of a group
+// and two 32-row blocks share each staged K/V tile, half the transfers per
+// product of 4-wave workgroups. Without grouping, 8 waves would be 256 rows
+// of one head, whose waves finish at different key tiles; 4 waves (two
+// workgroups per CU) measure as fast there.
+template <int D, bool CACHE>
+hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
+  return a.hq / a.hkv >= 2 ? launch_fwd_w<D, CACHE, 8>(a, stream)
+                           : launch_fwd_w<D, CACHE, 4>(a, stream);
 }
 
 }  // namespace
