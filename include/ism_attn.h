@@ -18,7 +18,8 @@
  *      q, o: [T, hq, d];  k, v: [T, hkv, d]   (T = tokens of the packed batch)
  *      lse:  [hq, T] float32, natural-log log-sum-exp of the scaled scores.
  *  - Grouped KV heads: query head h reads key/value head h / (hq / hkv);
- *    hq must be a multiple of hkv. Supported head dims: d = 64 and d = 128.
+ *    hq must be a multiple of hkv, hq <= 8192. Supported head dims: d = 64
+ *    and d = 128.
  *  - `scale` multiplies Q K^T before the softmax (normally 1/sqrt(d)).
  *  - All work is enqueued on `stream` (a hipStream_t passed as void*, NULL =
  *    the default stream). No call synchronises the device.

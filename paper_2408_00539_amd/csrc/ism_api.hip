@@ -49,6 +49,10 @@ ism_status check_heads(int32_t hq, int32_t hkv, int32_t d, float scale) {
                 hq, hkv);
   if (d != 64 && d != 128)
     return fail(ISM_ERR_UNSUPPORTED, "head dim %d not supported (64 or 128)", d);
+  // tile transfers address 64 rows of a token-major tensor with 32-bit byte
+  // offsets: 64 * hq * d * 2 bytes must stay below 2^31
+  if (hq > 8192)
+    return fail(ISM_ERR_UNSUPPORTED, "hq %d above the supported 8192 heads", hq);
   if (!(scale > 0.f) || !isfinite(scale))
     return fail(ISM_ERR_SHAPE, "scale must be finite and > 0 (got %g)", (double)scale);
   return ISM_OK;

@@ -125,6 +125,15 @@ __device__ __forceinline__ void dma_x4(const void *g, uint32_t lds_base) {
                : "v"(g), "s"(__builtin_amdgcn_readfirstlane(lds_base))
                : "memory", "m0");
 }
+// The same with a wave-uniform base address in SGPRs and a per-lane 32-bit
+// byte offset (the address is base + offset): no 64-bit address arithmetic
+// per transfer.
+__device__ __forceinline__ void dma_x4s(const void *base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+               : "memory", "m0");
+}
 __device__ __forceinline__ void dma_x1(const void *g, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
                :
@@ -163,17 +172,24 @@ struct DmaTile {
   static constexpr int T = ROWS / RPI;              // transfers per tile
   static constexpr int NI = (T + NW - 1) / NW;      // transfers per wave (max)
   static_assert(ROWS % RPI == 0, "tile rows must fill whole transfers");
-  uint32_t loff[NI];  // element offset of this lane's source chunk (full tile)
+  uint32_t loff[NI];  // byte offset of this lane's source chunk (full tile)
   int wave, lane;
 
+  // rs: row stride in elements; ROWS * rs * 2 bytes must fit in 32 bits
   __device__ __forceinline__ void init(int tid, int64_t rs) {
     wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     lane = tid & 63;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = (i * NW + wave) * RPI + lane / CPR;
-      loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz<D>(r)) * 8);
+      loff[i] = (uint32_t)(r * rs + ((lane % CPR) ^ swz<D>(r)) * 8) * 2u;
     }
+  }
+
+  // Transfer i (of NI) of this wave for a tile whose rows are all valid.
+  __device__ __forceinline__ void issue_one(const bf16_t *src, int i, bf16_t *lds) const {
+    const int q = i * NW + wave;
+    if (q < T) dma_x4s(src, loff[i], lds_addr(lds) + q * 1024);
   }
 
   // Rows [0, ROWS) of the tile starting at src (row stride rs elements); rows
@@ -185,7 +201,7 @@ struct DmaTile {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int q = i * NW + wave;
-        if (q < T) dma_x4(src + loff[i], lb + q * 1024);
+        if (q < T) dma_x4s(src, loff[i], lb + q * 1024);
       }
     } else {
 #pragma unroll
@@ -194,7 +210,7 @@ struct DmaTile {
         if (q >= T) continue;
         const int r = q * RPI + lane / CPR;
         const int rr = min(r, nvalid - 1);
-        dma_x4(src + (int64_t)rr * rs + ((lane % CPR) ^ swz<D>(r)) * 8, lb + q * 1024);
+        dma_x4s(src, (uint32_t)(rr * rs + ((lane % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
       }
     }
   }

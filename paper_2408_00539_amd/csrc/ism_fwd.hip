@@ -169,12 +169,12 @@ __device__ __forceinline__ void tile_pv(const char *vl, const SwzOffsets<D> &so,
 // are busy at the same time. Returns the fp32 row sum of P(t); mt receives
 // the (unmasked) row max of S(t+1). With LAST (a wave's last tile) there is
 // no S(t+1): the exponentials run alone, then the P V products.
-template <int D, bool LAST>
+template <int D, bool LAST, class Hook>
 __device__ __forceinline__ float step_block(const char *kl, const char *vl,
                                             const SwzOffsets<D> &so, const bf16x8 (&qf)[D / 16],
                                             const f32x16 (&cur)[2], f32x16 (&nxt)[2],
                                             f32x16 (&oacc)[D / 32], float sl2, float moff,
-                                            float &mt) {
+                                            float &mt, Hook &&hook) {
   constexpr int NKS = D / 16, NDB = D / 32;
   constexpr int NS = 2 * NKS, NP = 4 * NDB, N = NS + NP, LA = 3;
   constexpr int PPS = 16 / NS;  // probability pairs per S product
@@ -205,6 +205,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
       const int j = n - NS, kc = j / NDB, db = j % NDB;
       oacc[db] = mfma32x32x16(op[n], __builtin_bit_cast(bf16x8, w[kc >> 1][kc & 1]), oacc[db]);
     }
+    hook(n);  // n is a constant once the loop is unrolled
     if (n >= F && n + LA < N) op[n + LA] = read(n + LA);
     if (n < NS) {
 #pragma unroll
@@ -352,25 +353,35 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   }
   lds_barrier();  // every wave is done with K(0) before K(2) overwrites it
 
-  // Step t; LAST is the workgroup's last tile, which has no S(t+1): the
-  // waves whose last tile it is run the exponentials and P V only. (A wave
-  // whose last tile comes earlier computes an unused S(t+1) there, which
-  // keeps one code path inside the loop.)
-  auto step = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], int t, auto lastc) {
-    constexpr bool LAST = decltype(lastc)::value;
+  // Step t. MODE 0: K(t+2) and V(t+1) are full tiles, transferred one
+  // transfer every few products (a burst of transfers stalls the waves that
+  // issue them); MODE 1: the transfers at once (partial tiles near the end
+  // of the key range); MODE 2: the workgroup's last tile, which has no
+  // S(t+1) and no transfers, so the waves whose last tile it is run the
+  // exponentials and P V only. (A wave whose last tile comes earlier
+  // computes an unused S(t+1) there, which keeps one code path per loop.)
+  auto step = [&](f32x16 (&cur)[2], f32x16 (&nxt)[2], int t, auto modec) {
+    constexpr int MODE = decltype(modec)::value;
+    constexpr bool LAST = MODE == 2;
+    constexpr int NI = decltype(dma)::NI;
     const int c0 = key_begin + t * kBN;
-    if (!LAST) {
+    const bf16_t *ksrc = kt + 2 * tile_elems, *vsrc = vt + tile_elems;
+    if (MODE == 1 || (MODE == 0 && t >= nw)) {
       if (t + 2 < ntiles)
-        dma.issue(kt + 2 * tile_elems, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
-      dma.issue(vt + tile_elems, rs, key_hi - (c0 + kBN) + 1, sm.v[(t + 1) & 1]);
-      kt += tile_elems;
-      vt += tile_elems;
+        dma.issue(ksrc, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
+      dma.issue(vsrc, rs, key_hi - (c0 + kBN) + 1, sm.v[(t + 1) & 1]);
     }
     const char *kl = (const char *)sm.k[(t + 1) & 1];
     const char *vl = (const char *)sm.v[t & 1];
+    auto hook = [&](int n) __attribute__((always_inline)) {
+      if (MODE == 0 && n % 4 == 0 && n / 4 < 2 * NI) {
+        if (n / 4 < NI) dma.issue_one(ksrc, n / 4, sm.k[t & 1]);
+        else dma.issue_one(vsrc, n / 4 - NI, sm.v[(t + 1) & 1]);
+      }
+    };
     if (t < nw) {
       float mt;
-      l_run += step_block<D, LAST>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt);
+      l_run += step_block<D, LAST>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt, hook);
       if (!LAST && t + 1 < nw) {
         if (c0 + 2 * kBN - 1 > wave_lo) {  // S(t+1) crosses some row's bound
           tile_mask(nxt, c0 + kBN, hf, lim_r);
@@ -379,16 +390,26 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
         raise_max(mt, sl2, tau, m_run, l_run, oacc);
       }
     }
+    if (!LAST) {
+      kt += tile_elems;
+      vt += tile_elems;
+    }
     wait_vmem();
     __syncthreads();
   };
-  const std::false_type mid{};
-  for (int t = 0; t + 1 < ntiles; t += 2) {
-    step(sa, sb, t, mid);
-    if (t + 2 < ntiles) step(sb, sa, t + 1, mid);
+  // steps whose K(t+2) and V(t+1) are full tiles, an even count of them
+  const int nfull = max((key_hi - key_begin + 1) / kBN - 2, 0) & ~1;
+  int t = 0;
+  for (; t < nfull; t += 2) {
+    step(sa, sb, t, std::integral_constant<int, 0>{});
+    step(sb, sa, t + 1, std::integral_constant<int, 0>{});
   }
-  if ((ntiles - 1) & 1) step(sb, sa, ntiles - 1, std::true_type{});
-  else step(sa, sb, ntiles - 1, std::true_type{});
+  for (; t + 1 < ntiles; t += 2) {
+    step(sa, sb, t, std::integral_constant<int, 1>{});
+    if (t + 2 < ntiles) step(sb, sa, t + 1, std::integral_constant<int, 1>{});
+  }
+  if ((ntiles - 1) & 1) step(sb, sa, ntiles - 1, std::integral_constant<int, 2>{});
+  else step(sa, sb, ntiles - 1, std::integral_constant<int, 2>{});
 
   if (!active) return;
   const float lt = pair_sum(l_run);
