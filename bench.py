@@ -179,7 +179,8 @@ def bench_cache(w, timer, reps, warmup):
     out["decode"] = {"steps": w.steps, "ms_per_step": ms_turn / w.steps,
                      "gbs": b_dec / ms_turn / 1e6,
                      "frac_peak_hbm": b_dec / ms_turn / 1e6 / PEAK_HBM_GBS,
-                     "bytes": b_dec}
+                     "bytes": b_dec, "bytes_per_step": b_dec / w.steps,
+                     "traffic_per_step": recorded_decode_traffic()}
     return out
 
 
@@ -371,6 +372,99 @@ def recorded_traffic():
     return rec.get("bwd_bytes_per_launch")
 
 
+def _counter_means(path, counter):
+    """Mean per dispatch of one counter, per kernel, from a rocprofv3
+    counter_collection.csv (kernel name -> (mean KiB, dispatches))."""
+    import csv
+    sums, counts = {}, {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            k = _short_kernel(r["Kernel_Name"])
+            sums[k] = sums.get(k, 0.0) + float(r["Counter_Value"])
+            counts[k] = counts.get(k, 0) + 1
+    return {k: (sums[k] / counts[k], counts[k]) for k in sums}
+
+
+def _short_kernel(name):
+    import re
+    if name.startswith("_ZN3ism12_GLOBAL__N_1"):
+        rest = name[len("_ZN3ism12_GLOBAL__N_1"):]
+        m = re.match(r"(\d+)", rest)
+        n = int(m.group(1))
+        base = rest[len(m.group(1)):len(m.group(1)) + n]
+        t = re.match(r"ILi(\d+)E", rest[len(m.group(1)) + n:])
+        return base + (f"<{t.group(1)}>" if t else "")
+    name = name.replace("void ", "").replace("ism::(anonymous namespace)::", "")
+    return name.replace("ism::", "").split("(")[0]
+
+
+def write_traffic_record(fetch_copy, fetch_step, write_copy, write_step,
+                         fetch_cache=None, write_cache=None):
+    """Turn the counter passes into the traffic record bench.py reports:
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of each kernel, scaled by
+    what the same counters read for the plain COPY_BYTES copy."""
+    fc = _counter_means(fetch_copy, "FETCH_SIZE")
+    wc = _counter_means(write_copy, "WRITE_SIZE")
+    copy_f = max(v for v, _ in fc.values())
+    copy_w = max(v for v, _ in wc.values())
+    sf = COPY_BYTES / 1024 / copy_f
+    sw = COPY_BYTES / 1024 / copy_w
+    rec = {"kernel_source_sha256": kernel_source_hash(),
+           "workload": "training step, 8 dialogues x 4096 tokens, 32 heads, "
+                       "head_dim 128 (cache path: 32 x 8192, 32 heads)",
+           "copy_calibration": {"copy_bytes": COPY_BYTES,
+                                "FETCH_SIZE_KiB": round(copy_f, 1),
+                                "WRITE_SIZE_KiB": round(copy_w, 1),
+                                "scale_fetch": round(sf, 4),
+                                "scale_write": round(sw, 4)},
+           "kernels": {}}
+    passes = [(fetch_step, write_step)]
+    if fetch_cache and write_cache:
+        passes.append((fetch_cache, write_cache))
+    for fp, wp in passes:
+        fk, wk = _counter_means(fp, "FETCH_SIZE"), _counter_means(wp, "WRITE_SIZE")
+        for k in fk:
+            if k not in wk or "elementwise" in k or "copyBuffer" in k:
+                continue
+            f, w = fk[k][0], wk[k][0]
+            rec["kernels"][k] = {"FETCH_SIZE_KiB": round(f, 1),
+                                 "WRITE_SIZE_KiB": round(w, 1),
+                                 "bytes": int(sf * f * 1024 + sw * w * 1024)}
+    kb = rec["kernels"]
+    rec["bwd_bytes_per_launch"] = sum(
+        kb[k]["bytes"] for k in kb if k.startswith(("delta_kernel", "dkv_kernel", "dq_kernel")))
+    rec["fwd_bytes_per_launch"] = sum(
+        kb[k]["bytes"] for k in kb if k.startswith("fwd_kernel<128, false"))
+    dec = [k for k in kb if k.startswith("decode_split_kernel")]
+    if dec:
+        rec["decode_bytes_per_step"] = sum(kb[k]["bytes"] for k in kb
+                                           if k.startswith(("decode_split", "decode_combine")))
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    lines = ["| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (scaled) |",
+             "|---|---|---|---|"]
+    for k, v in kb.items():
+        lines.append(f"| {k} | {v['FETCH_SIZE_KiB']:.0f} | {v['WRITE_SIZE_KiB']:.0f} | "
+                     f"{v['bytes'] / 1e9:.3f} GB |")
+    print("\n".join(lines))
+    print(f"scale: fetch {sf:.3f}, write {sw:.3f}; backward {rec['bwd_bytes_per_launch'] / 1e9:.3f} GB"
+          f" per launch; sha256 {rec['kernel_source_sha256']}")
+
+
+def recorded_decode_traffic():
+    """HBM bytes per decode step from the counter record (or None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return rec.get("decode_bytes_per_step")
+
+
 def calibrate_copy():
     """A plain device copy of COPY_BYTES, ten times (for the counter scale)."""
     import torch
@@ -393,7 +487,15 @@ def main():
                                        "expansion", "latency"],
                     default="all")
     ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--write-traffic-record", nargs="+", metavar="CSV",
+                    help="counter_collection.csv files: FETCH_SIZE of the "
+                    "copy, of the step, WRITE_SIZE of the copy, of the step "
+                    "[, FETCH_SIZE and WRITE_SIZE of the cache path]; writes "
+                    "the traffic record (no GPU needed)")
     args = ap.parse_args()
+    if args.write_traffic_record:
+        write_traffic_record(*args.write_traffic_record)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU "
               "path (see the sharding design); run with --gpus 1",
