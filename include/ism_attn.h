@@ -160,6 +160,40 @@ ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            int32_t num_splits, void *ws, size_t ws_bytes,
                            void *stream);
 
+/* Paged KV cache: the same two operations with the cache held in fixed-size
+ * pages instead of one slab per dialogue, so that dialogues of very
+ * different lengths share one pool (the multi-turn serving case of Sec. 2.3,
+ * where every turn appends to the reused cache). k_pages / v_pages
+ * [num_pages, hkv, page_size, d] bf16; block_table [batch, max_pages] int32
+ * device: position t of dialogue b is slot t % page_size of page
+ * block_table[b * max_pages + t / page_size]. page_size must be a positive
+ * multiple of 64; a dialogue holds at most max_pages * page_size positions
+ * (this is cache_cap). The caller owns the pages and the table and
+ * allocates the pages a turn appends to before the call; table entries are
+ * read on the device and clamped into [0, num_pages). Results equal those
+ * of the dense entry points on the same logical cache. Workspaces as for
+ * ISM_OP_PREFILL_CACHED and ISM_OP_DECODE with cache_cap = max_pages *
+ * page_size. */
+ism_status ism_attn_prefill_paged(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
+    int32_t max_new, int32_t seg_is_query, const void *q_new,
+    const void *k_new, const void *v_new, void *k_pages, void *v_pages,
+    int32_t num_pages, int32_t page_size, const int32_t *block_table,
+    int32_t max_pages, const int32_t *cache_seqlens, void *o, float *lse,
+    int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+    size_t ws_bytes, void *stream);
+
+ism_status ism_attn_decode_paged(const void *q, const void *k_new,
+                                 const void *v_new, void *k_pages,
+                                 void *v_pages, int32_t num_pages,
+                                 int32_t page_size, const int32_t *block_table,
+                                 int32_t max_pages,
+                                 const int32_t *cache_seqlens, int32_t batch,
+                                 int32_t max_seqlen, void *o, float *lse,
+                                 int32_t hq, int32_t hkv, int32_t d,
+                                 float scale, int32_t num_splits, void *ws,
+                                 size_t ws_bytes, void *stream);
+
 /* Host-side validation of segment metadata (HOST pointers). Pure CPU, needs
  * no device. Returns ISM_OK or ISM_ERR_SEGMENTS / ISM_ERR_NULL /
  * ISM_ERR_SHAPE with the first violation in ism_last_error(). */

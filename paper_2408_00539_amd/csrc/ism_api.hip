@@ -214,16 +214,42 @@ extern "C" ism_status ism_attn_prefill_cached(
                                          ws_bytes, stream);
 }
 
-extern "C" ism_status ism_attn_prefill_cached_segment(
-    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
-    int32_t seg_is_query, const void *q_new, const void *k_new, const void *v_new,
-    void *k_cache, void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens, void *o,
-    float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
-    size_t ws_bytes, void *stream) {
+namespace {
+
+// A paged KV cache (see the paged entry points); null for a dense cache.
+struct Paging {
+  const int32_t *block_table;
+  int32_t max_pages, num_pages, page_size;
+};
+
+ism_status check_paging(const Paging &pg) {
+  if (!pg.block_table) return fail(ISM_ERR_NULL, "block_table is NULL");
+  if (pg.num_pages < 1 || pg.max_pages < 1)
+    return fail(ISM_ERR_SHAPE, "need num_pages >= 1 and max_pages >= 1 (got %d, %d)",
+                pg.num_pages, pg.max_pages);
+  if (pg.page_size < 64 || pg.page_size % 64 != 0)
+    return fail(ISM_ERR_UNSUPPORTED, "page_size %d is not a positive multiple of 64",
+                pg.page_size);
+  if ((int64_t)pg.max_pages * pg.page_size > INT32_MAX)
+    return fail(ISM_ERR_SHAPE, "max_pages * page_size exceeds the int32 position range");
+  return ISM_OK;
+}
+
+ism_status prefill_impl(const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
+                        int32_t max_new, int32_t seg_is_query, const void *q_new,
+                        const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+                        int32_t cache_cap, const int32_t *cache_seqlens, void *o, float *lse,
+                        int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+                        size_t ws_bytes, void *stream, const Paging *pg) {
   ism::clear_error();
   if (!cu_seqlens_new || !q_new || !k_new || !v_new || !k_cache || !v_cache ||
       !cache_seqlens || !o)
     return fail(ISM_ERR_NULL, "a required pointer is NULL");
+  if (pg) {
+    const ism_status ps = check_paging(*pg);
+    if (ps) return ps;
+    cache_cap = pg->max_pages * pg->page_size;
+  }
   if (batch < 1 || total_new < 1 || max_new < 1 || max_new > total_new)
     return fail(ISM_ERR_SHAPE,
                 "need batch >= 1, 1 <= max_new <= total_new (batch=%d total_new=%d "
@@ -236,11 +262,14 @@ extern "C" ism_status ism_attn_prefill_cached_segment(
   if ((st = check_device())) return st;
 
   hipStream_t s = (hipStream_t)stream;
-  if ((st = hip_status(ism::launch_cache_append(k_new, v_new, k_cache, v_cache,
-                                                cu_seqlens_new, cache_seqlens, batch,
-                                                max_new, hkv, d, cache_cap, s),
-                       "cache append launch")))
-    return st;
+  const hipError_t ae =
+      pg ? ism::launch_cache_append_paged(k_new, v_new, k_cache, v_cache, cu_seqlens_new,
+                                          cache_seqlens, pg->block_table, pg->max_pages,
+                                          pg->num_pages, pg->page_size, batch, max_new, hkv, d,
+                                          s)
+         : ism::launch_cache_append(k_new, v_new, k_cache, v_cache, cu_seqlens_new,
+                                    cache_seqlens, batch, max_new, hkv, d, cache_cap, s);
+  if ((st = hip_status(ae, "cache append launch"))) return st;
   ism::FwdArgs a{};
   a.q = q_new; a.k = k_cache; a.v = v_cache; a.o = o; a.lse = lse;
   a.cu_q = cu_seqlens_new;
@@ -254,20 +283,56 @@ extern "C" ism_status ism_attn_prefill_cached_segment(
   a.kv_row_stride = d;
   a.scale = scale;
   a.cache_causal = seg_is_query ? 0 : 1;
+  if (pg) {
+    a.block_table = pg->block_table;
+    a.max_pages = pg->max_pages;
+    a.num_pages = pg->num_pages;
+    a.page_size = pg->page_size;
+  }
   return hip_status(ism::launch_fwd(a, d, true, s), "cached prefill launch");
 }
 
-extern "C" ism_status ism_attn_decode(const void *q, const void *k_new,
-                                      const void *v_new, void *k_cache,
-                                      void *v_cache, int32_t cache_cap,
-                                      const int32_t *cache_seqlens, int32_t batch,
-                                      int32_t max_seqlen, void *o, float *lse,
-                                      int32_t hq, int32_t hkv, int32_t d, float scale,
-                                      int32_t num_splits, void *ws, size_t ws_bytes,
-                                      void *stream) {
+}  // namespace
+
+extern "C" ism_status ism_attn_prefill_cached_segment(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
+    int32_t seg_is_query, const void *q_new, const void *k_new, const void *v_new,
+    void *k_cache, void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens, void *o,
+    float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
+    size_t ws_bytes, void *stream) {
+  return prefill_impl(cu_seqlens_new, batch, total_new, max_new, seg_is_query, q_new, k_new,
+                      v_new, k_cache, v_cache, cache_cap, cache_seqlens, o, lse, hq, hkv, d,
+                      scale, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" ism_status ism_attn_prefill_paged(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
+    int32_t seg_is_query, const void *q_new, const void *k_new, const void *v_new,
+    void *k_pages, void *v_pages, int32_t num_pages, int32_t page_size,
+    const int32_t *block_table, int32_t max_pages, const int32_t *cache_seqlens, void *o,
+    float *lse, int32_t hq, int32_t hkv, int32_t d, float scale, void *ws, size_t ws_bytes,
+    void *stream) {
+  const Paging pg{block_table, max_pages, num_pages, page_size};
+  return prefill_impl(cu_seqlens_new, batch, total_new, max_new, seg_is_query, q_new, k_new,
+                      v_new, k_pages, v_pages, 0, cache_seqlens, o, lse, hq, hkv, d, scale, ws,
+                      ws_bytes, stream, &pg);
+}
+
+namespace {
+
+ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void *k_cache,
+                       void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens,
+                       int32_t batch, int32_t max_seqlen, void *o, float *lse, int32_t hq,
+                       int32_t hkv, int32_t d, float scale, int32_t num_splits, void *ws,
+                       size_t ws_bytes, void *stream, const Paging *pg) {
   ism::clear_error();
   if (!q || !k_new || !v_new || !k_cache || !v_cache || !cache_seqlens || !o)
     return fail(ISM_ERR_NULL, "a required pointer is NULL");
+  if (pg) {
+    const ism_status ps = check_paging(*pg);
+    if (ps) return ps;
+    cache_cap = pg->max_pages * pg->page_size;
+  }
   if (batch < 1 || cache_cap < 1)
     return fail(ISM_ERR_SHAPE, "need batch >= 1 and cache_cap >= 1");
   ism_status st = check_heads(hq, hkv, d, scale);
@@ -297,5 +362,40 @@ extern "C" ism_status ism_attn_decode(const void *q, const void *k_new,
   a.splits = splits;
   a.chunk = (max_seqlen + splits - 1) / splits;
   a.scale = scale;
+  if (pg) {
+    // a wave iteration's keys must lie in one page: chunks of 256 keys
+    a.chunk = (a.chunk + 255) / 256 * 256;
+    a.block_table = pg->block_table;
+    a.max_pages = pg->max_pages;
+    a.num_pages = pg->num_pages;
+    a.page_size = pg->page_size;
+  }
   return hip_status(ism::launch_decode(a, d, (hipStream_t)stream), "decode launch");
+}
+
+}  // namespace
+
+extern "C" ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
+                                      void *k_cache, void *v_cache, int32_t cache_cap,
+                                      const int32_t *cache_seqlens, int32_t batch,
+                                      int32_t max_seqlen, void *o, float *lse, int32_t hq,
+                                      int32_t hkv, int32_t d, float scale, int32_t num_splits,
+                                      void *ws, size_t ws_bytes, void *stream) {
+  return decode_impl(q, k_new, v_new, k_cache, v_cache, cache_cap, cache_seqlens, batch,
+                     max_seqlen, o, lse, hq, hkv, d, scale, num_splits, ws, ws_bytes, stream,
+                     nullptr);
+}
+
+extern "C" ism_status ism_attn_decode_paged(const void *q, const void *k_new,
+                                            const void *v_new, void *k_pages, void *v_pages,
+                                            int32_t num_pages, int32_t page_size,
+                                            const int32_t *block_table, int32_t max_pages,
+                                            const int32_t *cache_seqlens, int32_t batch,
+                                            int32_t max_seqlen, void *o, float *lse, int32_t hq,
+                                            int32_t hkv, int32_t d, float scale,
+                                            int32_t num_splits, void *ws, size_t ws_bytes,
+                                            void *stream) {
+  const Paging pg{block_table, max_pages, num_pages, page_size};
+  return decode_impl(q, k_new, v_new, k_pages, v_pages, 0, cache_seqlens, batch, max_seqlen, o,
+                     lse, hq, hkv, d, scale, num_splits, ws, ws_bytes, stream, &pg);
 }

@@ -39,7 +39,33 @@ cache_append_kernel(const bf16_t *__restrict__ k_src,
   *(u32x4 *)(v_cache + dst) = *(const u32x4 *)(v_src + src);
 }
 
-template <int D, int G>
+__global__ void __launch_bounds__(256)
+cache_append_paged_kernel(const bf16_t *__restrict__ k_src, const bf16_t *__restrict__ v_src,
+                          bf16_t *__restrict__ k_pages, bf16_t *__restrict__ v_pages,
+                          const int32_t *__restrict__ cu_new,
+                          const int32_t *__restrict__ cache_len,
+                          const int32_t *__restrict__ block_table, int32_t max_pages,
+                          int32_t num_pages, int32_t page_size, int32_t hkv, int32_t d) {
+  const int b = blockIdx.y;
+  const int r0 = cu_new[b], n = cu_new[b + 1] - r0;
+  const int cpr = hkv * (d / 8);
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)n * cpr) return;
+  const int r = (int)(idx / cpr), rem = (int)(idx % cpr);
+  const int pos = cache_len[b] + r;
+  if (pos < 0 || pos >= max_pages * page_size) return;  // out of contract
+  const int h = rem / (d / 8), c = rem % (d / 8);
+  const int64_t src = ((int64_t)(r0 + r) * hkv + h) * d + c * 8;
+  const int64_t dst =
+      paged_offset(block_table, max_pages, num_pages, page_size, hkv, d, b, h, pos) + c * 8;
+  *(u32x4 *)(k_pages + dst) = *(const u32x4 *)(k_src + src);
+  *(u32x4 *)(v_pages + dst) = *(const u32x4 *)(v_src + src);
+}
+
+// Split decode step. PAGED: the cache is a page pool (DecodeArgs); the keys
+// of one wave iteration (KPW consecutive, KPW-aligned: chunks are multiples
+// of 256) lie in one page, whose address is looked up once per iteration.
+template <int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
   constexpr int CPK = D / 8;     // lanes per key row (16 bytes each)
@@ -61,17 +87,23 @@ decode_split_kernel(DecodeArgs a) {
   const int owner = min(p / a.chunk, a.splits - 1);
   const float sl2 = a.scale * kLog2e;
 
+  // element offset of key t's row (dense slab or page pool)
   const int64_t slab = ((int64_t)b * a.hkv + kvh) * a.cap * D;
-  const bf16_t *kc = (const bf16_t *)a.k_cache + slab + c * 8;
-  const bf16_t *vc = (const bf16_t *)a.v_cache + slab + c * 8;
+  auto row_of = [&](int t) -> int64_t {
+    if (PAGED)
+      return paged_offset_uniform(a.block_table, a.max_pages, a.num_pages, a.page_size, a.hkv,
+                                  D, b, kvh, t);
+    return slab + (int64_t)t * D;
+  };
   const bf16_t *kn = (const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
   const bf16_t *vn = (const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
 
   if (split == owner && tid < CPK) {
     // this chunk owns the new token: store it into the cache
-    *(u32x4 *)((bf16_t *)a.k_cache + slab + (int64_t)p * D + tid * 8) =
+    const int64_t prow = row_of(p);
+    *(u32x4 *)((bf16_t *)a.k_cache + prow + tid * 8) =
         *(const u32x4 *)((const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
-    *(u32x4 *)((bf16_t *)a.v_cache + slab + (int64_t)p * D + tid * 8) =
+    *(u32x4 *)((bf16_t *)a.v_cache + prow + tid * 8) =
         *(const u32x4 *)((const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
   }
 
@@ -97,6 +129,10 @@ decode_split_kernel(DecodeArgs a) {
 
   for (int base = k0 + wave * KPW; base < k1; base += 4 * KPW) {
     u32x4 kr[U], vr[U];
+    // keys [base, base + KPW) of this iteration: one page when paged
+    const int64_t brow = row_of(base) - (int64_t)base * D;
+    const bf16_t *kc = (const bf16_t *)a.k_cache + brow + c * 8;
+    const bf16_t *vc = (const bf16_t *)a.v_cache + brow + c * 8;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int key = min(base + u * KPI + slot, p);
@@ -219,8 +255,12 @@ decode_combine_kernel(DecodeArgs a) {
 
 template <int D, int G>
 hipError_t launch_decode_t(const DecodeArgs &a, hipStream_t stream) {
-  hipLaunchKernelGGL((decode_split_kernel<D, G>),
-                     dim3(a.splits, a.hkv, a.batch), dim3(256), 0, stream, a);
+  if (a.block_table)
+    hipLaunchKernelGGL((decode_split_kernel<D, G, true>), dim3(a.splits, a.hkv, a.batch),
+                       dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_split_kernel<D, G, false>), dim3(a.splits, a.hkv, a.batch),
+                       dim3(256), 0, stream, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(a.batch * a.hq), dim3(D),
@@ -252,6 +292,21 @@ hipError_t launch_cache_append(const void *k_src, const void *v_src,
                      dim3(256), 0, stream, (const bf16_t *)k_src,
                      (const bf16_t *)v_src, (bf16_t *)k_cache, (bf16_t *)v_cache,
                      cu_new, cache_len, hkv, d, cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_append_paged(const void *k_src, const void *v_src, void *k_pages,
+                                     void *v_pages, const int32_t *cu_new,
+                                     const int32_t *cache_len, const int32_t *block_table,
+                                     int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                     int32_t batch, int32_t max_new, int32_t hkv, int32_t d,
+                                     hipStream_t stream) {
+  const int64_t chunks = (int64_t)max_new * hkv * (d / 8);
+  if (chunks == 0 || batch == 0) return hipSuccess;
+  hipLaunchKernelGGL(cache_append_paged_kernel, dim3((unsigned)((chunks + 255) / 256), batch),
+                     dim3(256), 0, stream, (const bf16_t *)k_src, (const bf16_t *)v_src,
+                     (bf16_t *)k_pages, (bf16_t *)v_pages, cu_new, cache_len, block_table,
+                     max_pages, num_pages, page_size, hkv, d);
   return hipGetLastError();
 }
 

@@ -232,7 +232,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
   return sum[0] + sum[1];
 }
 
-template <int D, bool CACHE, int NWV>
+template <int D, bool CACHE, int NWV, bool PAGED>
 __global__ void __launch_bounds__(NWV * 64)
 __attribute__((amdgpu_waves_per_eu(ISM_FWD_WPE, ISM_FWD_WPE)))
 fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
@@ -269,7 +269,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     cache_c = a.cache_len[b];
     // keys [0, C_b + L_b) (query segment) or [0, C_b + r] for row r (answer
     // segment); clamped to the slab for out-of-contract lengths
-    const int slab_rows = (int)(a.kv_head_stride / D);
+    const int slab_rows = PAGED ? a.max_pages * a.page_size : (int)(a.kv_head_stride / D);
     if (a.cache_causal) {
       key_hi = max(min(cache_c + (wg_last - s) + 1, slab_rows) - 1, 0);
       wave_lo = min(cache_c + (min(wq0, e - 1) - s), key_hi);
@@ -279,7 +279,8 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
       wave_lo = key_hi;
       wave_hi = active ? key_hi : -1;
     }
-    const int64_t off = (int64_t)b * a.kv_seq_stride + (int64_t)kvh * a.kv_head_stride;
+    const int64_t off =
+        PAGED ? 0 : (int64_t)b * a.kv_seq_stride + (int64_t)kvh * a.kv_head_stride;
     kbase = (const bf16_t *)a.k + off;
     vbase = (const bf16_t *)a.v + off;
   } else {
@@ -292,6 +293,16 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   }
   const int64_t rs = a.kv_row_stride;
   const float sl2 = a.scale * kLog2e;
+  // first key of tile t of the workgroup's key range (t < its tile count);
+  // in the paged cache a 64-key tile lies inside one page
+  const int32_t *btab = a.block_table;
+  const int pg_max = a.max_pages, pg_num = a.num_pages, pg_size = a.page_size, nkv = a.hkv;
+  auto tile_src = [&](const bf16_t *base, int t) __attribute__((always_inline)) {
+    if constexpr (PAGED)
+      return base + paged_offset_uniform(btab, pg_max, pg_num, pg_size, nkv, D, b, kvh, t * kBN);
+    else
+      return base + (int64_t)key_begin * rs + (int64_t)t * (kBN * rs);
+  };
   // lazy rescale threshold: 2^8 in probability units
   const float tau = 8.f / sl2;
 
@@ -303,11 +314,12 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   dma.init(tid, rs);
   {
     const int mem_rows = CACHE ? key_hi - key_begin + 1 : e - key_begin;
-    const bf16_t *k0 = kbase + (int64_t)key_begin * rs;
-    const bf16_t *v0 = vbase + (int64_t)key_begin * rs;
+    const bf16_t *k0 = tile_src(kbase, 0);
     dma.issue(k0, rs, mem_rows, sm.k[0]);
-    dma.issue(v0, rs, mem_rows, sm.v[0]);
-    if (mem_rows > kBN) dma.issue(k0 + (int64_t)kBN * rs, rs, mem_rows - kBN, sm.k[1]);
+    dma.issue(tile_src(vbase, 0), rs, mem_rows, sm.v[0]);
+    if (mem_rows > kBN)
+      dma.issue(PAGED ? tile_src(kbase, 1) : k0 + (int64_t)kBN * rs, rs, mem_rows - kBN,
+                sm.k[1]);
   }
   // Per-lane query row (clamped into the dialogue; rows past e are computed
   // as copies of the last row and never stored).
@@ -342,6 +354,9 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   const int64_t tile_elems = (int64_t)kBN * rs;
   const bf16_t *kt = kbase + (int64_t)key_begin * rs;
   const bf16_t *vt = vbase + (int64_t)key_begin * rs;
+  // paged cache: sources of K(t+2) and V(t+1) for step t
+  const bf16_t *pk2 = PAGED ? tile_src(kbase, min(2, ntiles - 1)) : kt;
+  const bf16_t *pv1 = PAGED ? tile_src(vbase, min(1, ntiles - 1)) : vt;
   SwzOffsets<D> so;
   so.init(lane);
 
@@ -365,7 +380,8 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     constexpr bool LAST = MODE == 2;
     constexpr int NI = decltype(dma)::NI;
     const int c0 = key_begin + t * kBN;
-    const bf16_t *ksrc = kt + 2 * tile_elems, *vsrc = vt + tile_elems;
+    const bf16_t *ksrc = PAGED ? pk2 : kt + 2 * tile_elems;
+    const bf16_t *vsrc = PAGED ? pv1 : vt + tile_elems;
     if (MODE == 1 || (MODE == 0 && t >= nw)) {
       if (t + 2 < ntiles)
         dma.issue(ksrc, rs, key_hi - (c0 + 2 * kBN) + 1, sm.k[t & 1]);
@@ -393,16 +409,25 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     if (!LAST) {
       kt += tile_elems;
       vt += tile_elems;
+      if constexpr (PAGED) {  // K(t+3) and V(t+2), re-based at page starts
+        const int tpp = pg_size / kBN;
+        pk2 = (t + 3) % tpp ? pk2 + tile_elems : tile_src(kbase, min(t + 3, ntiles - 1));
+        pv1 = (t + 2) % tpp ? pv1 + tile_elems : tile_src(vbase, min(t + 2, ntiles - 1));
+      }
     }
     wait_vmem();
     __syncthreads();
   };
   // steps whose K(t+2) and V(t+1) are full tiles, an even count of them
-  const int nfull = max((key_hi - key_begin + 1) / kBN - 2, 0) & ~1;
+  // (the paged cache looks up each tile's page at the step start and issues
+  // its transfers at once)
   int t = 0;
-  for (; t < nfull; t += 2) {
-    step(sa, sb, t, std::integral_constant<int, 0>{});
-    step(sb, sa, t + 1, std::integral_constant<int, 0>{});
+  if constexpr (!PAGED) {
+    const int nfull = max((key_hi - key_begin + 1) / kBN - 2, 0) & ~1;
+    for (; t < nfull; t += 2) {
+      step(sa, sb, t, std::integral_constant<int, 0>{});
+      step(sb, sa, t + 1, std::integral_constant<int, 0>{});
+    }
   }
   for (; t + 1 < ntiles; t += 2) {
     step(sa, sb, t, std::integral_constant<int, 1>{});
@@ -434,14 +459,14 @@ int gcd_int(int x, int y) {
   return x;
 }
 
-template <int D, bool CACHE, int NWV>
+template <int D, bool CACHE, int NWV, bool PAGED>
 hipError_t launch_fwd_w(const FwdArgs &a, hipStream_t stream) {
   const int hpw = gcd_int(a.hq / a.hkv, NWV);
   const int wg_rows = (NWV / hpw) * kQW;
   const int tiles = (a.max_rows + wg_rows - 1) / wg_rows;
   const int64_t groups = (int64_t)a.batch * (a.hq / hpw);
   if (groups * tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((fwd_kernel<D, CACHE, NWV>), dim3((unsigned)xcd_grid(groups, tiles)),
+  hipLaunchKernelGGL((fwd_kernel<D, CACHE, NWV, PAGED>), dim3((unsigned)xcd_grid(groups, tiles)),
                      dim3(NWV * 64), 0, stream, a, hpw, tiles, ISM_SCHED_CHUNK);
   return hipGetLastError();
 }
@@ -451,10 +476,16 @@ hipError_t launch_fwd_w(const FwdArgs &a, hipStream_t stream) {
 // product of 4-wave workgroups. Without grouping, 8 waves would be 256 rows
 // of one head, whose waves finish at different key tiles; 4 waves (two
 // workgroups per CU) measure as fast there.
+template <int D, bool CACHE, bool PAGED>
+hipError_t launch_fwd_p(const FwdArgs &a, hipStream_t stream) {
+  return a.hq / a.hkv >= 2 ? launch_fwd_w<D, CACHE, 8, PAGED>(a, stream)
+                           : launch_fwd_w<D, CACHE, 4, PAGED>(a, stream);
+}
+
 template <int D, bool CACHE>
 hipError_t launch_fwd_t(const FwdArgs &a, hipStream_t stream) {
-  return a.hq / a.hkv >= 2 ? launch_fwd_w<D, CACHE, 8>(a, stream)
-                           : launch_fwd_w<D, CACHE, 4>(a, stream);
+  if (CACHE && a.block_table) return launch_fwd_p<D, true, true>(a, stream);
+  return launch_fwd_p<D, CACHE, false>(a, stream);
 }
 
 }  // namespace

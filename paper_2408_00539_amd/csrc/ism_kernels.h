@@ -33,6 +33,11 @@ struct FwdArgs {
   float scale;
   int32_t cache_causal;     // cache mode: the new segment is an answer
                             // segment (row r sees keys [0, C_b + r])
+  // paged cache mode: k / v are page pools [num_pages, hkv, page_size, d];
+  // key t of dialogue b is slot t % page_size of page
+  // block_table[b * max_pages + t / page_size] (page_size % 64 == 0)
+  const int32_t *block_table;
+  int32_t page_size, max_pages, num_pages;
 };
 
 hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
@@ -42,6 +47,30 @@ hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
 hipError_t launch_fwd(const FwdArgs &a, int d, bool cache_mode,
                       hipStream_t stream);
 
+// Paged cache: where token position t of dialogue b lives. The page index is
+// clamped into the pool so that a bad table entry never addresses memory
+// outside it. Returns the element offset of (page, head h, slot, 0).
+__device__ __forceinline__ int64_t paged_offset(const int32_t *block_table, int32_t max_pages,
+                                                int32_t num_pages, int32_t page_size,
+                                                int32_t hkv, int32_t d, int b, int h, int t) {
+  int page = block_table[(int64_t)b * max_pages + t / page_size];
+  page = min(max(page, 0), num_pages - 1);
+  return (((int64_t)page * hkv + h) * page_size + t % page_size) * d;
+}
+
+// The same for a position that is the same in every lane of the wave (a
+// scalar load of the table entry, the offset in scalar registers).
+__device__ __forceinline__ int64_t paged_offset_uniform(const int32_t *block_table,
+                                                        int32_t max_pages, int32_t num_pages,
+                                                        int32_t page_size, int32_t hkv,
+                                                        int32_t d, int b, int h, int t) {
+  const int idx = __builtin_amdgcn_readfirstlane(b * max_pages + t / page_size);
+  int page = __builtin_amdgcn_readfirstlane(block_table[idx]);
+  page = min(max(page, 0), num_pages - 1);
+  return (((int64_t)page * hkv + h) * page_size + __builtin_amdgcn_readfirstlane(t % page_size)) *
+         d;
+}
+
 // Cache append: rows [cu_new[b], cu_new[b+1]) of src go to positions
 // cache_len[b] + (r - cu_new[b]) of slab b. src is [Tn, hkv, d];
 // cache is [batch, hkv, cap, d].
@@ -50,6 +79,15 @@ hipError_t launch_cache_append(const void *k_src, const void *v_src,
                                const int32_t *cu_new, const int32_t *cache_len,
                                int32_t batch, int32_t max_new, int32_t hkv,
                                int32_t d, int32_t cap, hipStream_t stream);
+
+// The same into a paged cache (layout as in FwdArgs); cap = max_pages *
+// page_size positions per dialogue.
+hipError_t launch_cache_append_paged(const void *k_src, const void *v_src, void *k_pages,
+                                     void *v_pages, const int32_t *cu_new,
+                                     const int32_t *cache_len, const int32_t *block_table,
+                                     int32_t max_pages, int32_t num_pages, int32_t page_size,
+                                     int32_t batch, int32_t max_new, int32_t hkv, int32_t d,
+                                     hipStream_t stream);
 
 struct DecodeArgs {
   const void *q;            // [batch, hq, d]
@@ -64,6 +102,9 @@ struct DecodeArgs {
   float *part_ml;           // [batch, hq, splits, 2]
   int32_t batch, hq, hkv, cap, splits, chunk;
   float scale;
+  // paged cache (see FwdArgs); chunk is then a multiple of 256
+  const int32_t *block_table;
+  int32_t page_size, max_pages, num_pages;
 };
 
 hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream);

@@ -7,7 +7,8 @@ fallback: if the library is not built or no gfx950 device is present, the
 call fails loudly.
 
 Names follow the C ABI (include/ism_attn.h): fwd, bwd, prefill_cached,
-prefill_cached_segment, decode, plus check_segments_host and workspace_size.
+prefill_cached_segment, decode, prefill_paged, decode_paged, plus
+check_segments_host and workspace_size.
 """
 
 from __future__ import annotations
@@ -58,6 +59,12 @@ _SIGS = {
     "ism_attn_prefill_cached_segment": (_I, [_P, _I, _I, _I, _I, _P, _P, _P,
                                              _P, _P, _I, _P, _P, _P, _I, _I,
                                              _I, _F, _P, _Z, _P]),
+    "ism_attn_prefill_paged": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P,
+                                    _I, _I, _P, _I, _P, _P, _P, _I, _I, _I,
+                                    _F, _P, _Z, _P]),
+    "ism_attn_decode_paged": (_I, [_P, _P, _P, _P, _P, _I, _I, _P, _I, _P,
+                                   _I, _I, _P, _P, _I, _I, _I, _F, _I, _P,
+                                   _Z, _P]),
     "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
                              _I, _I, _F, _I, _P, _Z, _P]),
     "ism_check_segments_host": (_I, [_P, _P, _P, _I, _I, _I, _I]),
@@ -307,3 +314,73 @@ def check_segments_host(cu_seqlens, cu_segs, seg_is_query, max_seqlen=None):
         cu.ctypes.data, cs.ctypes.data, fl.ctypes.data, len(cu) - 1, len(fl),
         int(cu[-1]) if len(cu) else 0, ms)
     return st, lib().ism_last_error().decode()
+
+
+def _need_pages(k_pages, v_pages, block_table, hkv, d):
+    torch = _torch()
+    P, hk, ps, dd = k_pages.shape
+    _need(k_pages, "k_pages", torch.bfloat16, (P, hkv, ps, d))
+    _need(v_pages, "v_pages", torch.bfloat16, (P, hkv, ps, d))
+    _need(block_table, "block_table", torch.int32)
+    if block_table.dim() != 2:
+        raise ValueError("block_table must be [batch, max_pages]")
+    return P, ps, block_table.shape[1]
+
+
+def prefill_paged(q_new, k_new, v_new, k_pages, v_pages, block_table,
+                  cache_seqlens, cu_seqlens_new, max_new, seg_is_query=True,
+                  scale=None, return_lse=True):
+    """New segment against a paged cache (appends k_new/v_new into the
+    pages block_table names). k_pages/v_pages [P, hkv, page_size, d] bf16,
+    block_table [B, max_pages] int32. Returns (o, lse)."""
+    torch = _torch()
+    Tn, hq, d = q_new.shape
+    hkv = k_new.shape[1]
+    P, ps, mp = _need_pages(k_pages, v_pages, block_table, hkv, d)
+    B = block_table.shape[0]
+    _need(q_new, "q_new", torch.bfloat16)
+    _need(k_new, "k_new", torch.bfloat16, (Tn, hkv, d))
+    _need(v_new, "v_new", torch.bfloat16, (Tn, hkv, d))
+    _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
+    _need(cu_seqlens_new, "cu_seqlens_new", torch.int32, (B + 1,))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q_new)
+    lse = torch.empty((hq, Tn), dtype=torch.float32, device=q_new.device) \
+        if return_lse else None
+    _check(lib().ism_attn_prefill_paged(
+        _ptr(cu_seqlens_new), B, Tn, int(max_new), int(bool(seg_is_query)),
+        _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
+        P, ps, _ptr(block_table), mp, _ptr(cache_seqlens), _ptr(o), _ptr(lse),
+        hq, hkv, d, scale, None, 0, _stream()))
+    return o, lse
+
+
+def decode_paged(q, k_new, v_new, k_pages, v_pages, block_table,
+                 cache_seqlens, max_seqlen=0, scale=None, num_splits=0,
+                 return_lse=True, workspace=None):
+    """One decode step against a paged cache (appends k_new/v_new at
+    cache_seqlens[b]). Returns (o [B,hq,d] bf16, lse [hq,B] fp32 or None)."""
+    torch = _torch()
+    B, hq, d = q.shape
+    hkv = k_new.shape[1]
+    P, ps, mp = _need_pages(k_pages, v_pages, block_table, hkv, d)
+    _need(q, "q", torch.bfloat16)
+    _need(k_new, "k_new", torch.bfloat16, (B, hkv, d))
+    _need(v_new, "v_new", torch.bfloat16, (B, hkv, d))
+    _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
+    if block_table.shape[0] != B:
+        raise ValueError("block_table rows != batch")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    cap = mp * ps
+    ms = cap if not max_seqlen else int(max_seqlen)
+    nws = workspace_size(ISM_OP_DECODE, B, 0, ms, hq, hkv, d, num_splits)
+    ws = workspace if workspace is not None else _workspace(nws, q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((hq, B), dtype=torch.float32, device=q.device) \
+        if return_lse else None
+    _check(lib().ism_attn_decode_paged(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages), P, ps,
+        _ptr(block_table), mp, _ptr(cache_seqlens), B, int(max_seqlen),
+        _ptr(o), _ptr(lse), hq, hkv, d, scale, int(num_splits), _ptr(ws),
+        nws if workspace is None else workspace.numel(), _stream()))
+    return o, lse

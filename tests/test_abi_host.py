@@ -143,6 +143,18 @@ def test_cache_argument_errors(L):
         assert L.ism_attn_prefill_cached_segment(
             FAKE, 1, 10, 10, flag, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE,
             None, None, 1, 1, 64, 0.125, None, 0, None) == 1
+    # paged cache: page size not a multiple of 64, no table, empty pool
+    for ps, tab, npages, want in ((96, FAKE, 4, 3), (64, None, 4, 1), (64, FAKE, 0, 2)):
+        assert L.ism_attn_prefill_paged(
+            FAKE, 1, 10, 10, 1, FAKE, FAKE, FAKE, FAKE, FAKE, npages, ps, tab, 2, FAKE,
+            FAKE, None, 1, 1, 64, 0.125, None, 0, None) == want
+        assert L.ism_attn_decode_paged(
+            FAKE, FAKE, FAKE, FAKE, FAKE, npages, ps, tab, 2, FAKE, 1, 0, FAKE, None,
+            1, 1, 64, 0.125, 0, ws, 1 << 20, None) == want
+    # paged prefill: new segment longer than max_pages * page_size
+    assert L.ism_attn_prefill_paged(
+        FAKE, 1, 200, 200, 1, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 64, FAKE, 2, FAKE, FAKE,
+        None, 1, 1, 64, 0.125, None, 0, None) == 6
     # bwd: null gradient output
     sg = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
     assert L.ism_attn_bwd(ctypes.byref(sg), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
