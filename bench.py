@@ -181,6 +181,38 @@ def bench_cache(w, timer, reps, warmup):
                      "frac_peak_hbm": b_dec / ms_turn / 1e6 / PEAK_HBM_GBS,
                      "bytes": b_dec, "bytes_per_step": b_dec / w.steps,
                      "traffic_per_step": recorded_decode_traffic()}
+
+    # the same turn through a paged cache: pages of 256 positions scattered
+    # over a shuffled pool, one block table row per dialogue
+    ps = 256
+    mp = w.cache_cap // ps
+    npages = B * mp + 64
+    g = torch.Generator(device="cpu").manual_seed(1234)
+    table = torch.randperm(npages, generator=g)[:B * mp].to(torch.int32).view(B, mp).cuda()
+
+    def to_pages(c):
+        pool = torch.zeros((npages, w.hkv, ps, w.d), dtype=c.dtype, device=c.device)
+        pool[table.view(-1).long()] = (c.view(B, w.hkv, mp, ps, w.d).permute(0, 2, 1, 3, 4)
+                                       .reshape(B * mp, w.hkv, ps, w.d))
+        return pool
+    Kp, Vp = to_pages(Kc), to_pages(Vc)
+    ms_pp = timer.run(lambda: ops.prefill_paged(qn, kn, vn, Kp, Vp, table, lens, cu, mx,
+                                                True, w.scale), reps, warmup)
+    out["prefill_paged"] = {"ms": ms_pp, "page_size": ps,
+                            "tflops": f_pf / ms_pp / 1e9,
+                            "vs_dense": ms_pf / ms_pp}
+
+    def turn_paged():
+        pos = pos0.clone()
+        for t in range(w.steps):
+            ops.decode_paged(qd[t], kd[t], vd[t], Kp, Vp, table, pos, 0, w.scale,
+                             workspace=ws)
+            pos += 1
+    ms_tp = timer.run(turn_paged, max(1, reps // 4), 1)
+    out["decode_paged"] = {"ms_per_step": ms_tp / w.steps, "page_size": ps,
+                           "gbs": b_dec / ms_tp / 1e6,
+                           "frac_peak_hbm": b_dec / ms_tp / 1e6 / PEAK_HBM_GBS,
+                           "vs_dense": ms_turn / ms_tp}
     return out
 
 
@@ -439,8 +471,11 @@ def write_traffic_record(fetch_copy, fetch_step, write_copy, write_step,
         kb[k]["bytes"] for k in kb if k.startswith("fwd_kernel<128, false"))
     dec = [k for k in kb if k.startswith("decode_split_kernel")]
     if dec:
-        rec["decode_bytes_per_step"] = sum(kb[k]["bytes"] for k in kb
-                                           if k.startswith(("decode_split", "decode_combine")))
+        # the dense cache's kernels (the paged ones carry PAGED = true)
+        rec["decode_bytes_per_step"] = sum(
+            kb[k]["bytes"] for k in kb
+            if k.startswith("decode_combine")
+            or (k.startswith("decode_split") and "true" not in k))
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(rec, f, indent=1)
     lines = ["| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (scaled) |",

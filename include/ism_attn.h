@@ -145,8 +145,9 @@ ism_status ism_attn_prefill_cached_segment(
  * and itself). For dialogue b the new token sits at position
  * p_b = cache_seqlens[b]: its key/value (k_new / v_new [batch, hkv, d]) are
  * written into the cache at p_b, then q [batch, hq, d] attends to keys
- * [0, p_b]. The key range is split into `num_splits` chunks processed in
- * parallel and merged exactly (0 = choose automatically). o [batch, hq, d]
+ * [0, p_b]. Each dialogue's key range is split into `num_splits` chunks of
+ * equal length (0 = choose automatically), processed in parallel and merged
+ * exactly. o [batch, hq, d]
  * bf16; lse [hq, batch] fp32 or NULL. The caller guarantees p_b < cache_cap
  * and advances cache_seqlens by 1 afterwards. max_seqlen bounds p_b + 1 for
  * the split choice (0 = cache_cap). Workspace: ism_attn_workspace_size(

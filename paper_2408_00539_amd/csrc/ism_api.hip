@@ -360,11 +360,8 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
   a.part_ml = (float *)((char *)ws + align_up((size_t)batch * hq * splits * d * 4));
   a.batch = batch; a.hq = hq; a.hkv = hkv; a.cap = cache_cap;
   a.splits = splits;
-  a.chunk = (max_seqlen + splits - 1) / splits;
   a.scale = scale;
   if (pg) {
-    // a wave iteration's keys must lie in one page: chunks of 256 keys
-    a.chunk = (a.chunk + 255) / 256 * 256;
     a.block_table = pg->block_table;
     a.max_pages = pg->max_pages;
     a.num_pages = pg->num_pages;

@@ -62,9 +62,14 @@ cache_append_paged_kernel(const bf16_t *__restrict__ k_src, const bf16_t *__rest
   *(u32x4 *)(v_pages + dst) = *(const u32x4 *)(v_src + src);
 }
 
-// Split decode step. PAGED: the cache is a page pool (DecodeArgs); the keys
-// of one wave iteration (KPW consecutive, KPW-aligned: chunks are multiples
-// of 256) lie in one page, whose address is looked up once per iteration.
+// Split decode step. Each dialogue's key range [0, p] is cut into a.splits
+// chunks of equal length rounded up to a whole workgroup iteration (4 KPW
+// keys), so every chunk but the last runs whole iterations and the longest
+// chunk is as short as the split count allows, whatever the cache capacity;
+// trailing chunks of a short dialogue may be empty (partial m = -inf, l = 0).
+// PAGED: the cache is a page pool (DecodeArgs); the keys of one wave
+// iteration (KPW consecutive, KPW-aligned) lie in one page, whose address
+// is looked up once per iteration.
 template <int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
@@ -81,10 +86,13 @@ decode_split_kernel(DecodeArgs a) {
   // position of the new token; clamped so that out-of-contract positions
   // never address memory outside the slab
   const int p = min(max(a.pos[b], 0), a.cap - 1);
-  // the last chunk runs to p even if the host's bound on p was too small
-  const int k0 = split * a.chunk;
-  const int k1 = split == a.splits - 1 ? p + 1 : min(k0 + a.chunk, p + 1);
-  const int owner = min(p / a.chunk, a.splits - 1);
+  // chunk * splits >= p + 1, so the chunks cover [0, p] and p / chunk is a
+  // valid split
+  constexpr int kGran = 4 * KPW;
+  const int chunk = ((p + a.splits) / a.splits + kGran - 1) / kGran * kGran;
+  const int k0 = split * chunk;
+  const int k1 = min(k0 + chunk, p + 1);
+  const int owner = p / chunk;
   const float sl2 = a.scale * kLog2e;
 
   // element offset of key t's row (dense slab or page pool)

@@ -100,9 +100,9 @@ struct DecodeArgs {
   float *lse;               // [hq, batch] or null
   float *part_o;            // [batch, hq, splits, d]
   float *part_ml;           // [batch, hq, splits, 2]
-  int32_t batch, hq, hkv, cap, splits, chunk;
+  int32_t batch, hq, hkv, cap, splits;
   float scale;
-  // paged cache (see FwdArgs); chunk is then a multiple of 256
+  // paged cache (see FwdArgs)
   const int32_t *block_table;
   int32_t page_size, max_pages, num_pages;
 };
