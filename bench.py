@@ -54,6 +54,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_step_8x4096_h32_d128.json
 COPY_BYTES = 1 << 30  # --calibrate-copy: bytes read (and written) per copy
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
+WARM_MS = 200.0      # warmup floor of the paths' measurements (Timer.run)
+LAT_WARM_MS = 20.0   # the same for the latency experiment's short launches
 
 
 def log(*a):
@@ -94,10 +96,18 @@ class Timer:
         self.a = torch.cuda.Event(enable_timing=True)
         self.b = torch.cuda.Event(enable_timing=True)
 
-    def run(self, fn, reps, warmup):
+    def run(self, fn, reps, warmup, warm_ms=0.0):
+        """Mean ms of ``reps`` calls after ``warmup`` untimed calls and, with
+        ``warm_ms``, further untimed calls until that much time has passed
+        (after an idle stretch, such as a host-to-device upload, the clock
+        needs some tens of ms of work to ramp back up)."""
         for _ in range(warmup):
             fn()
         self.torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        while (time.perf_counter() - t0) * 1e3 < warm_ms:
+            fn()
+            self.torch.cuda.synchronize()
         self.a.record()
         for _ in range(reps):
             fn()
@@ -117,14 +127,15 @@ def bench_training(w, timer, steps, warmup, with_bwd):
     f_bwd = 10 * w.d * w.hq * pairs
     res = {"visible_pairs_per_head": pairs}
     o, lse = ops.fwd(q, k, v, segs, w.scale)
-    ms_fwd = timer.run(lambda: ops.fwd(q, k, v, segs, w.scale), steps, warmup)
+    ms_fwd = timer.run(lambda: ops.fwd(q, k, v, segs, w.scale), steps, warmup,
+                       WARM_MS)
     res["fwd"] = {"ms": ms_fwd, "tflops": f_fwd / ms_fwd / 1e9,
                   "frac_peak": f_fwd / ms_fwd / 1e9 / PEAK_BF16_TFLOPS,
                   "flop": f_fwd}
     if with_bwd:
         do = dev(w.do) if w.do is not None else torch.randn_like(q)
         ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale),
-                           steps, warmup)
+                           steps, warmup, WARM_MS)
         res["bwd"] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
                       "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
                       "flop": f_bwd}
@@ -150,7 +161,7 @@ def bench_cache(w, timer, reps, warmup):
     mx = int(w.new_lens.max())
     L = w.new_lens.astype(np.int64)
     ms_pf = timer.run(lambda: ops.prefill_cached(qn, kn, vn, Kc, Vc, lens, cu,
-                                                 mx, w.scale), reps, warmup)
+                                                 mx, w.scale), reps, warmup, WARM_MS)
     f_pf = 4 * w.d * w.hq * float(np.sum(L * (w.hist_len + L)))
     b_pf = 2 * w.hkv * w.d * 2 * float(np.sum(w.hist_len + L))
     out = {"prefill_cached": {
@@ -173,7 +184,7 @@ def bench_cache(w, timer, reps, warmup):
             ops.decode(qd[t], kd[t], vd[t], Kc, Vc, pos, 0, w.scale,
                        workspace=ws)
             pos += 1
-    ms_turn = timer.run(turn, max(1, reps // 4), 1)
+    ms_turn = timer.run(turn, max(1, reps // 4), 1, WARM_MS)
     keys = float(np.sum([np.sum(w.hist_len + L + t + 1) for t in range(w.steps)]))
     b_dec = 2 * w.hkv * w.d * 2 * keys
     out["decode"] = {"steps": w.steps, "ms_per_step": ms_turn / w.steps,
@@ -197,7 +208,7 @@ def bench_cache(w, timer, reps, warmup):
         return pool
     Kp, Vp = to_pages(Kc), to_pages(Vc)
     ms_pp = timer.run(lambda: ops.prefill_paged(qn, kn, vn, Kp, Vp, table, lens, cu, mx,
-                                                True, w.scale), reps, warmup)
+                                                True, w.scale), reps, warmup, WARM_MS)
     out["prefill_paged"] = {"ms": ms_pp, "page_size": ps,
                             "tflops": f_pf / ms_pp / 1e9,
                             "vs_dense": ms_pf / ms_pp}
@@ -208,7 +219,7 @@ def bench_cache(w, timer, reps, warmup):
             ops.decode_paged(qd[t], kd[t], vd[t], Kp, Vp, table, pos, 0, w.scale,
                              workspace=ws)
             pos += 1
-    ms_tp = timer.run(turn_paged, max(1, reps // 4), 1)
+    ms_tp = timer.run(turn_paged, max(1, reps // 4), 1, WARM_MS)
     out["decode_paged"] = {"ms_per_step": ms_tp / w.steps, "page_size": ps,
                            "gbs": b_dec / ms_tp / 1e6,
                            "frac_peak_hbm": b_dec / ms_tp / 1e6 / PEAK_HBM_GBS,
@@ -236,7 +247,7 @@ def bench_expansion(w, timer, reps, warmup, ism_step_ms):
     def step():
         o, lse = ops.fwd(q, k, v, segs, w.scale)
         ops.bwd(q, k, v, o, lse, do, segs, w.scale)
-    ms = timer.run(step, reps, warmup)
+    ms = timer.run(step, reps, warmup, WARM_MS)
     return {"train_prefix_expansion": {
         "workload": "the dialogues of the training step, one sample per turn",
         "samples": exp.batch, "tokens": exp.total, "ms": ms,
@@ -289,7 +300,8 @@ def bench_latency(timer, reps=5, seed=5):
         clen = torch.full((B,), C, dtype=torch.int32, device="cuda")
         for mode, isq in (("ttft_ism_ms", True), ("ttft_causal_ms", False)):
             out[mode].append(timer.run(lambda: ops.prefill_cached_segment(
-                qn, kn, vn, kc, vc, clen, cu_new, LAT_Q, isq, scale), reps, 2))
+                qn, kn, vn, kc, vc, clen, cu_new, LAT_Q, isq, scale), reps, 2,
+                LAT_WARM_MS))
         # prefix mask: the whole prefix, one bidirectional segment per dialogue
         cu = np.arange(B + 1, dtype=np.int32) * P
         psegs = ops.Segments.from_host(cu, cu, np.ones(B, np.uint8))
@@ -297,7 +309,7 @@ def bench_latency(timer, reps=5, seed=5):
         kp = K[:, :P].reshape(B * P, LAT_HKV, LAT_D).contiguous()
         vp = V[:, :P].reshape(B * P, LAT_HKV, LAT_D).contiguous()
         out["ttft_prefix_ms"].append(timer.run(
-            lambda: ops.fwd(qp, kp, vp, psegs, scale), reps, 2))
+            lambda: ops.fwd(qp, kp, vp, psegs, scale), reps, 2, LAT_WARM_MS))
         del qp, kp, vp
         # the answer, one token per step
         qd = Q[:, P:C + LAT_Q + LAT_A].transpose(0, 1).contiguous()
@@ -310,7 +322,8 @@ def bench_latency(timer, reps=5, seed=5):
             for t in range(LAT_A):
                 ops.decode(qd[t], kd[t], vd[t], kc, vc, pos[t], T_ctx, scale,
                            workspace=ws)
-        out["tpot_ms"].append(timer.run(answer, 1, 0) / LAT_A)
+        # (a repeated answer writes the same keys to the same positions)
+        out["tpot_ms"].append(timer.run(answer, 1, 1, LAT_WARM_MS) / LAT_A)
     res = {"workload": f"{B} dialogues x {LAT_TURNS} turns x ({LAT_Q} query + "
                        f"{LAT_A} answer) tokens, {LAT_HQ}/{LAT_HKV} heads, "
                        f"head_dim {LAT_D}, one attention layer",
