@@ -164,13 +164,17 @@ __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" 
 // by the NW waves of a workgroup. Each global_load_lds_dwordx4 writes lane
 // l's 16 bytes to LDS bytes [16 l, 16 l + 16) of a 1 KB block, so the swizzle
 // is applied by choosing each lane's source chunk. No registers hold the
-// data. Block q of the tile is issued by wave q % NW.
+// data. Block q of the tile is issued by wave q % NW; the workgroup has
+// exactly NW waves.
 template <int D, int ROWS, int NW = 4>
 struct DmaTile {
   static constexpr int CPR = D / 8;                 // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;              // rows per 1 KB transfer
   static constexpr int T = ROWS / RPI;              // transfers per tile
   static constexpr int NI = (T + NW - 1) / NW;      // transfers per wave (max)
+  // every wave issues NI transfers (no per-transfer bound check, which the
+  // compiler would keep as a branch around each transfer)
+  static constexpr bool kEven = T % NW == 0;
   static_assert(ROWS % RPI == 0, "tile rows must fill whole transfers");
   uint32_t loff[NI];  // byte offset of this lane's source chunk (full tile)
   int wave, lane;
@@ -189,7 +193,7 @@ struct DmaTile {
   // Transfer i (of NI) of this wave for a tile whose rows are all valid.
   __device__ __forceinline__ void issue_one(const bf16_t *src, int i, bf16_t *lds) const {
     const int q = i * NW + wave;
-    if (q < T) dma_x4s(src, loff[i], lds_addr(lds) + q * 1024);
+    if (kEven || q < T) dma_x4s(src, loff[i], lds_addr(lds) + q * 1024);
   }
 
   // Rows [0, ROWS) of the tile starting at src (row stride rs elements); rows
@@ -201,13 +205,13 @@ struct DmaTile {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int q = i * NW + wave;
-        if (q < T) dma_x4s(src, loff[i], lb + q * 1024);
+        if (kEven || q < T) dma_x4s(src, loff[i], lb + q * 1024);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int q = i * NW + wave;
-        if (q >= T) continue;
+        if (!kEven && q >= T) continue;
         const int r = q * RPI + lane / CPR;
         const int rr = min(r, nvalid - 1);
         dma_x4s(src, (uint32_t)(rr * rs + ((lane % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
