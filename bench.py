@@ -224,6 +224,22 @@ def bench_cache(w, timer, reps, warmup):
                            "gbs": b_dec / ms_tp / 1e6,
                            "frac_peak_hbm": b_dec / ms_tp / 1e6 / PEAK_HBM_GBS,
                            "vs_dense": ms_turn / ms_tp}
+
+    # verification of drafted tokens (speculative decoding): the first
+    # n_draft decode inputs of every dialogue as one causal answer chunk
+    # through the paged cache, against n_draft decode steps
+    n_draft = 8
+    cu_d = torch.arange(B + 1, dtype=torch.int32, device="cuda") * n_draft
+
+    def chunk(x):
+        return x[:n_draft].transpose(0, 1).reshape(B * n_draft, *x.shape[2:]).contiguous()
+    qv, kv, vv = chunk(qd), chunk(kd), chunk(vd)
+    ms_ver = timer.run(lambda: ops.prefill_paged(qv, kv, vv, Kp, Vp, table, pos0, cu_d,
+                                                 n_draft, False, w.scale), reps, warmup,
+                       WARM_MS)
+    out["verify_paged"] = {"drafts": n_draft, "ms": ms_ver,
+                           "decode_steps_ms": n_draft * ms_tp / w.steps,
+                           "speedup_vs_decode": n_draft * ms_tp / w.steps / ms_ver}
     return out
 
 
