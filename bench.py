@@ -240,6 +240,27 @@ def bench_cache(w, timer, reps, warmup):
     out["verify_paged"] = {"drafts": n_draft, "ms": ms_ver,
                            "decode_steps_ms": n_draft * ms_tp / w.steps,
                            "speedup_vs_decode": n_draft * ms_tp / w.steps / ms_ver}
+
+    # ChatGLM-style 2-D positions (the new query is the dialogue's segment
+    # 2 x 16 = 32, offsets 0..L-1): the prefill with the rotation fused into
+    # the append and the query load, against rotating q and k first
+    p1 = torch.full((qn.shape[0],), 32, dtype=torch.int32, device="cuda")
+    p2 = torch.cat([torch.arange(int(n), dtype=torch.int32) for n in w.new_lens]).cuda()
+    ms_rf = timer.run(lambda: ops.prefill_cached_rope2d(qn, kn, vn, Kc, Vc, lens, cu, mx,
+                                                        p1, p2, True, scale=w.scale),
+                      reps, warmup, WARM_MS)
+    qr, kr = qn.clone(), kn.clone()
+
+    def unfused():
+        ops.rope2d_(qr, p1, p2)
+        ops.rope2d_(kr, p1, p2)
+        ops.prefill_cached_segment(qr, kr, vn, Kc, Vc, lens, cu, mx, True, w.scale)
+    ms_ru = timer.run(unfused, reps, warmup, WARM_MS)
+    ms_rq = timer.run(lambda: ops.rope2d_(qr, p1, p2), reps, warmup, WARM_MS)
+    rq_bytes = 2 * qr.numel() * 2  # bf16 read + write
+    out["prefill_rope2d"] = {"fused_ms": ms_rf, "unfused_ms": ms_ru, "plain_ms": ms_pf,
+                             "rope_q_ms": ms_rq, "rope_q_gbs": rq_bytes / ms_rq / 1e6,
+                             "rope_q_frac_peak_hbm": rq_bytes / ms_rq / 1e6 / PEAK_HBM_GBS}
     return out
 
 

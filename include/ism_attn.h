@@ -195,6 +195,56 @@ ism_status ism_attn_decode_paged(const void *q, const void *k_new,
                                  float scale, int32_t num_splits, void *ws,
                                  size_t ws_bytes, void *stream);
 
+/* ChatGLM-style 2-D rotary positions, kept when ISM is adapted to a
+ * prefix-style backbone (Sec. 2.3: one position encodes the span a token
+ * belongs to, the other its offset inside the span; bidirectional attention
+ * within query spans, causal within answer spans). Dims [0, d/2) of every
+ * head rotate by pos1, dims [d/2, d) by pos2; inside a half of width
+ * r = d/2, dims k and k + r/2 (k < r/2) form a pair rotated by the angle
+ * pos * base^(-2k/r): x_k' = x_k cos a - x_{k+r/2} sin a,
+ * x_{k+r/2}' = x_k sin a + x_{k+r/2} cos a. Angles are formed in fp32
+ * revolutions (relative error about 2^-23: ~1e-3 rad at pos * base^(-2k/r)
+ * = 10^4) and their fraction goes to the hardware sine / cosine; values are
+ * rotated in fp32 and rounded to bf16 (round to nearest even) for bf16
+ * tensors. */
+enum { ISM_DTYPE_BF16 = 0, ISM_DTYPE_F32 = 1 };
+
+/* Positions of a packed batch from its segments: pos1[j] = index of j's
+ * segment counted from its dialogue's first segment, pos2[j] = j minus the
+ * first token of its segment. pos1, pos2 [total_tokens] int32 device,
+ * written. */
+ism_status ism_positions_2d(const ism_segments *sg, int32_t *pos1,
+                            int32_t *pos2, void *stream);
+
+/* In-place rotation of x [total, heads, d] (device; dtype ISM_DTYPE_BF16 or
+ * ISM_DTYPE_F32) by the positions pos1, pos2 [total] int32 (device) of its
+ * tokens; d is 64 or 128; base finite and > 1 (10000 in ChatGLM).
+ * `inverse` != 0 rotates by minus the angle: applied to fp32 gradients with
+ * respect to rotated queries / keys (ism_attn_bwd on rotated inputs) it
+ * gives the gradients with respect to the unrotated ones. Training with the
+ * positions: rotate q and k, ism_attn_fwd, ism_attn_bwd, then rotate dq and
+ * dk back. */
+ism_status ism_rope2d(void *x, int32_t dtype, int32_t total, int32_t heads,
+                      int32_t d, const int32_t *pos1, const int32_t *pos2,
+                      float base, int32_t inverse, void *stream);
+
+/* ism_attn_prefill_cached_segment with the new tokens' 2-D positions
+ * pos1_new, pos2_new [total_new] int32 (device): the new keys are rotated on
+ * their way into the cache (which therefore holds rotated keys, as a
+ * rotary-position cache does) and each new query row is rotated as the
+ * attention loads it; values are not rotated. Equal, bit for bit, to
+ * ism_rope2d on q_new and k_new followed by
+ * ism_attn_prefill_cached_segment. Dense cache only; a decode step with
+ * positions rotates its q and k_new with ism_rope2d first. */
+ism_status ism_attn_prefill_cached_rope2d(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
+    int32_t max_new, int32_t seg_is_query, const void *q_new,
+    const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+    int32_t cache_cap, const int32_t *cache_seqlens, const int32_t *pos1_new,
+    const int32_t *pos2_new, float rope_base, void *o, float *lse, int32_t hq,
+    int32_t hkv, int32_t d, float scale, void *ws, size_t ws_bytes,
+    void *stream);
+
 /* Host-side validation of segment metadata (HOST pointers). Pure CPU, needs
  * no device. Returns ISM_OK or ISM_ERR_SEGMENTS / ISM_ERR_NULL /
  * ISM_ERR_SHAPE with the first violation in ism_last_error(). */

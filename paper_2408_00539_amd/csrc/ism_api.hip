@@ -235,12 +235,26 @@ ism_status check_paging(const Paging &pg) {
   return ISM_OK;
 }
 
+// 2-D rotary positions of the new tokens (see the rope entry points); null
+// for none.
+struct Rope {
+  const int32_t *pos1, *pos2;
+  float base;
+};
+
+ism_status check_rope_base(float base) {
+  if (!(base > 1.f) || !isfinite(base))
+    return fail(ISM_ERR_SHAPE, "rope base %g must be finite and > 1", (double)base);
+  return ISM_OK;
+}
+
 ism_status prefill_impl(const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
                         int32_t max_new, int32_t seg_is_query, const void *q_new,
                         const void *k_new, const void *v_new, void *k_cache, void *v_cache,
                         int32_t cache_cap, const int32_t *cache_seqlens, void *o, float *lse,
                         int32_t hq, int32_t hkv, int32_t d, float scale, void *ws,
-                        size_t ws_bytes, void *stream, const Paging *pg) {
+                        size_t ws_bytes, void *stream, const Paging *pg,
+                        const Rope *rp = nullptr) {
   ism::clear_error();
   if (!cu_seqlens_new || !q_new || !k_new || !v_new || !k_cache || !v_cache ||
       !cache_seqlens || !o)
@@ -258,12 +272,20 @@ ism_status prefill_impl(const int32_t *cu_seqlens_new, int32_t batch, int32_t to
   if (st) return st;
   if (cache_cap < max_new)
     return fail(ISM_ERR_CAPACITY, "cache_cap %d < max_new %d", cache_cap, max_new);
+  if (rp) {
+    if (!rp->pos1 || !rp->pos2) return fail(ISM_ERR_NULL, "pos1_new and pos2_new are required");
+    if ((st = check_rope_base(rp->base))) return st;
+  }
   (void)ws; (void)ws_bytes;
   if ((st = check_device())) return st;
 
   hipStream_t s = (hipStream_t)stream;
+  const float l2b = rp ? log2f(rp->base) : 0.f;
   const hipError_t ae =
-      pg ? ism::launch_cache_append_paged(k_new, v_new, k_cache, v_cache, cu_seqlens_new,
+      rp ? ism::launch_cache_append_rope(k_new, v_new, k_cache, v_cache, cu_seqlens_new,
+                                         cache_seqlens, rp->pos1, rp->pos2, l2b, batch, max_new,
+                                         hkv, d, cache_cap, s)
+      : pg ? ism::launch_cache_append_paged(k_new, v_new, k_cache, v_cache, cu_seqlens_new,
                                           cache_seqlens, pg->block_table, pg->max_pages,
                                           pg->num_pages, pg->page_size, batch, max_new, hkv, d,
                                           s)
@@ -289,6 +311,11 @@ ism_status prefill_impl(const int32_t *cu_seqlens_new, int32_t batch, int32_t to
     a.num_pages = pg->num_pages;
     a.page_size = pg->page_size;
   }
+  if (rp) {
+    a.rope_pos1 = rp->pos1;
+    a.rope_pos2 = rp->pos2;
+    a.rope_log2_base = l2b;
+  }
   return hip_status(ism::launch_fwd(a, d, true, s), "cached prefill launch");
 }
 
@@ -303,6 +330,50 @@ extern "C" ism_status ism_attn_prefill_cached_segment(
   return prefill_impl(cu_seqlens_new, batch, total_new, max_new, seg_is_query, q_new, k_new,
                       v_new, k_cache, v_cache, cache_cap, cache_seqlens, o, lse, hq, hkv, d,
                       scale, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" ism_status ism_attn_prefill_cached_rope2d(
+    const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new, int32_t max_new,
+    int32_t seg_is_query, const void *q_new, const void *k_new, const void *v_new,
+    void *k_cache, void *v_cache, int32_t cache_cap, const int32_t *cache_seqlens,
+    const int32_t *pos1_new, const int32_t *pos2_new, float rope_base, void *o, float *lse,
+    int32_t hq, int32_t hkv, int32_t d, float scale, void *ws, size_t ws_bytes, void *stream) {
+  const Rope rp{pos1_new, pos2_new, rope_base};
+  return prefill_impl(cu_seqlens_new, batch, total_new, max_new, seg_is_query, q_new, k_new,
+                      v_new, k_cache, v_cache, cache_cap, cache_seqlens, o, lse, hq, hkv, d,
+                      scale, ws, ws_bytes, stream, nullptr, &rp);
+}
+
+extern "C" ism_status ism_positions_2d(const ism_segments *sg, int32_t *pos1, int32_t *pos2,
+                                       void *stream) {
+  ism::clear_error();
+  ism_status st = check_segments(sg);
+  if (st) return st;
+  if (!pos1 || !pos2) return fail(ISM_ERR_NULL, "pos1 and pos2 are required");
+  if ((st = check_device())) return st;
+  return hip_status(ism::launch_positions_2d(sg->cu_seqlens, sg->batch, sg->cu_segs,
+                                             sg->num_segs, sg->total_tokens, pos1, pos2,
+                                             (hipStream_t)stream),
+                    "positions launch");
+}
+
+extern "C" ism_status ism_rope2d(void *x, int32_t dtype, int32_t total, int32_t heads,
+                                 int32_t d, const int32_t *pos1, const int32_t *pos2,
+                                 float base, int32_t inverse, void *stream) {
+  ism::clear_error();
+  if (!x || !pos1 || !pos2) return fail(ISM_ERR_NULL, "x, pos1 and pos2 are required");
+  if (dtype != ISM_DTYPE_BF16 && dtype != ISM_DTYPE_F32)
+    return fail(ISM_ERR_UNSUPPORTED, "dtype %d is neither ISM_DTYPE_BF16 nor ISM_DTYPE_F32",
+                dtype);
+  if (total < 0 || heads < 0)
+    return fail(ISM_ERR_SHAPE, "total %d and heads %d must be >= 0", total, heads);
+  if (d != 64 && d != 128) return fail(ISM_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+  ism_status st = check_rope_base(base);
+  if (st) return st;
+  if ((st = check_device())) return st;
+  return hip_status(ism::launch_rope2d(x, dtype == ISM_DTYPE_F32, total, heads, d, pos1, pos2,
+                                       log2f(base), inverse != 0, (hipStream_t)stream),
+                    "rope launch");
 }
 
 extern "C" ism_status ism_attn_prefill_paged(

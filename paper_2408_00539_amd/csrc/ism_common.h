@@ -358,4 +358,41 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) {
   return __builtin_bit_cast(float, w & 0xffff0000u);
 }
 
+// ChatGLM-style 2-D rotary positions (kept when ISM is adapted to a
+// prefix-style backbone, Sec. 2.3): dims [0, d/2) of a head rotate by the
+// token's span position pos1, dims [d/2, d) by its offset position pos2;
+// inside a half of width r = d/2, dims k and k + r/2 (k < r/2) form a pair
+// rotated by the angle pos * base^(-2k/r). Every path that rotates (the
+// in-place kernel, the fused cache append, the forward's query load) uses
+// these two functions, so they give identical bf16 results.
+// The angle is formed in revolutions (pos * base^(-2k/r) / 2 pi, two fp32
+// roundings: a relative error of about 2^-23, as forming the angle in fp32
+// radians has), and its fraction goes to the hardware sine / cosine, which
+// take revolutions: a few instructions instead of a range-reduced sincosf.
+__device__ __forceinline__ void rope_cs(int pos, int k, int r, float log2_base, float &c,
+                                        float &s) {
+  // 2k / r is exact (r is a power of two)
+  const float freq_rev = exp2f(-((float)(2 * k) / (float)r) * log2_base) * 0.159154943091895f;
+  const float rev = __builtin_amdgcn_fractf((float)pos * freq_rev);
+  s = __builtin_amdgcn_sinf(rev);
+  c = __builtin_amdgcn_cosf(rev);
+}
+
+// Rotate 8 pairs: dims of chunk a with the dims r/2 further in chunk b (8
+// bf16 each), angles given by c[i], s[i] (s negated for the inverse).
+__device__ __forceinline__ void rope_rotate8(u32x4 &a, u32x4 &b, const float (&c)[8],
+                                             const float (&s)[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float x0 = bf16_lo(a[i]), x1 = bf16_hi(a[i]);
+    float y0 = bf16_lo(b[i]), y1 = bf16_hi(b[i]);
+    const float u0 = fmaf(x0, c[2 * i], -(y0 * s[2 * i]));
+    const float v0 = fmaf(x0, s[2 * i], y0 * c[2 * i]);
+    const float u1 = fmaf(x1, c[2 * i + 1], -(y1 * s[2 * i + 1]));
+    const float v1 = fmaf(x1, s[2 * i + 1], y1 * c[2 * i + 1]);
+    a[i] = pack_bf16x2(u0, u1);
+    b[i] = pack_bf16x2(v0, v1);
+  }
+}
+
 }  // namespace ism

@@ -66,6 +66,30 @@ struct FwdSmem {
   bf16_t v[2][kBN * D];
 };
 
+// 2-D rotary positions of one query row held as MFMA operands: qf[ks] holds
+// dims 16 ks + 8 hf .. + 7, so each pair (k, k + D/4) of a half lies in
+// qf[ks] and qf[ks + D/64] of the same lane.
+template <int D>
+__device__ __forceinline__ void rope_queries(bf16x8 (&qf)[D / 16], int hf, int p1, int p2,
+                                             float log2_base) {
+  constexpr int NKS = D / 16, QK = NKS / 4;  // k steps per quarter of the head
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+#pragma unroll
+    for (int j = 0; j < QK; ++j) {
+      const int ks = half * (NKS / 2) + j;
+      const int ci = 2 * j + hf;  // 8-dim chunk inside the half's first quarter
+      float c[8], s[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) rope_cs(half ? p2 : p1, ci * 8 + e, D / 2, log2_base, c[e], s[e]);
+      u32x4 x = __builtin_bit_cast(u32x4, qf[ks]), y = __builtin_bit_cast(u32x4, qf[ks + QK]);
+      rope_rotate8(x, y, c, s);
+      qf[ks] = __builtin_bit_cast(bf16x8, x);
+      qf[ks + QK] = __builtin_bit_cast(bf16x8, y);
+    }
+  }
+}
+
 // S^T[key][row] = K Q^T for one 64-key tile: two 32-key blocks, D/16 steps.
 template <int D>
 __device__ __forceinline__ void tile_scores(const char *kl, const SwzOffsets<D> &so,
@@ -332,6 +356,9 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     const bf16_t *qp = (const bf16_t *)a.q + ((int64_t)rc * a.hq + head) * D + hf * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qf[ks] = *(const bf16x8 *)(qp + ks * 16);
+  }
+  if constexpr (CACHE) {
+    if (a.rope_pos1) rope_queries<D>(qf, hf, a.rope_pos1[rc], a.rope_pos2[rc], a.rope_log2_base);
   }
   wait_loads();  // Q, lim and the transfers above
   __syncthreads();

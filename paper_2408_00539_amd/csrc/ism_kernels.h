@@ -38,6 +38,10 @@ struct FwdArgs {
   // block_table[b * max_pages + t / page_size] (page_size % 64 == 0)
   const int32_t *block_table;
   int32_t page_size, max_pages, num_pages;
+  // cache mode: 2-D rotary positions of the new rows (null = none); each
+  // query row is rotated as it is loaded (the keys were rotated on append)
+  const int32_t *rope_pos1, *rope_pos2;
+  float rope_log2_base;
 };
 
 hipError_t launch_prep_lim(const int32_t *cu_segs, const uint8_t *seg_is_query,
@@ -130,5 +134,21 @@ hipError_t launch_bwd_prep(const int32_t *cu_segs, const uint8_t *seg_is_query,
                            hipStream_t stream);
 
 hipError_t launch_bwd(const BwdArgs &a, int d, hipStream_t stream);
+
+// 2-D rotary positions (ism_rope.hip): positions from the segment layout,
+// in-place rotation of [total, heads, d] (bf16 or fp32; inverse rotates by
+// minus the angle), and the dense cache append with the keys rotated.
+hipError_t launch_positions_2d(const int32_t *cu_seqlens, int32_t batch, const int32_t *cu_segs,
+                               int32_t num_segs, int32_t total, int32_t *pos1, int32_t *pos2,
+                               hipStream_t stream);
+hipError_t launch_rope2d(void *x, bool fp32, int32_t total, int32_t heads, int32_t d,
+                         const int32_t *pos1, const int32_t *pos2, float log2_base,
+                         bool inverse, hipStream_t stream);
+hipError_t launch_cache_append_rope(const void *k_src, const void *v_src, void *k_cache,
+                                    void *v_cache, const int32_t *cu_new,
+                                    const int32_t *cache_len, const int32_t *pos1,
+                                    const int32_t *pos2, float log2_base, int32_t batch,
+                                    int32_t max_new, int32_t hkv, int32_t d, int32_t cap,
+                                    hipStream_t stream);
 
 }  // namespace ism

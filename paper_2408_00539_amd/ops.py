@@ -21,6 +21,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libism_attn.so")
 
 ISM_OP_FWD, ISM_OP_BWD, ISM_OP_PREFILL_CACHED, ISM_OP_DECODE = range(4)
+ISM_DTYPE_BF16, ISM_DTYPE_F32 = range(2)
+ROPE_BASE = 10000.0
 STATUS = {0: "ISM_OK", 1: "ISM_ERR_NULL", 2: "ISM_ERR_SHAPE",
           3: "ISM_ERR_UNSUPPORTED", 4: "ISM_ERR_SEGMENTS",
           5: "ISM_ERR_WORKSPACE", 6: "ISM_ERR_CAPACITY",
@@ -67,6 +69,12 @@ _SIGS = {
                                    _Z, _P]),
     "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
                              _I, _I, _F, _I, _P, _Z, _P]),
+    "ism_positions_2d": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P]),
+    "ism_rope2d": (_I, [_P, _I, _I, _I, _I, _P, _P, _F, _I, _P]),
+    "ism_attn_prefill_cached_rope2d": (_I, [_P, _I, _I, _I, _I, _P, _P, _P,
+                                            _P, _P, _I, _P, _P, _P, _F, _P,
+                                            _P, _I, _I, _I, _F, _P, _Z,
+                                            _P]),
     "ism_check_segments_host": (_I, [_P, _P, _P, _I, _I, _I, _I]),
     "ism_status_string": (ctypes.c_char_p, [_I]),
     "ism_last_error": (ctypes.c_char_p, []),
@@ -270,6 +278,69 @@ def _prefill(seg_is_query, q_new, k_new, v_new, k_cache, v_cache,
             _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
             _ptr(v_cache), cap, _ptr(cache_seqlens), _ptr(o), _ptr(lse), hq,
             hkv, d, scale, None, 0, _stream()))
+    return o, lse
+
+
+def positions_2d(segs):
+    """2-D positions (pos1 = segment index in the dialogue, pos2 = offset in
+    the segment) of every token of a packed batch: two int32 [T] tensors."""
+    torch = _torch()
+    dev = segs.cu_seqlens.device
+    pos1 = torch.empty(segs.total_tokens, dtype=torch.int32, device=dev)
+    pos2 = torch.empty_like(pos1)
+    st = segs.c_struct()
+    _check(lib().ism_positions_2d(ctypes.byref(st), _ptr(pos1), _ptr(pos2), _stream()))
+    return pos1, pos2
+
+
+def rope2d_(x, pos1, pos2, base=ROPE_BASE, inverse=False):
+    """Rotate x [T, heads, d] (bf16 or fp32) in place by the 2-D positions
+    pos1, pos2 [T] int32; ``inverse`` rotates back (for gradients)."""
+    torch = _torch()
+    if x.dim() != 3 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [T, heads, d] tensor")
+    if x.dtype == torch.bfloat16:
+        dt = ISM_DTYPE_BF16
+    elif x.dtype == torch.float32:
+        dt = ISM_DTYPE_F32
+    else:
+        raise ValueError(f"x must be bf16 or fp32, got {x.dtype}")
+    T, H, d = x.shape
+    _need(pos1, "pos1", torch.int32, (T,))
+    _need(pos2, "pos2", torch.int32, (T,))
+    _check(lib().ism_rope2d(_ptr(x), dt, T, H, d, _ptr(pos1), _ptr(pos2), float(base),
+                            int(bool(inverse)), _stream()))
+    return x
+
+
+def prefill_cached_rope2d(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
+                          cu_seqlens_new, max_new, pos1_new, pos2_new,
+                          seg_is_query=True, base=ROPE_BASE, scale=None,
+                          return_lse=True):
+    """prefill_cached_segment with the new tokens' 2-D positions: keys are
+    rotated into the cache, queries as they are loaded (q_new and k_new
+    themselves are left unrotated)."""
+    torch = _torch()
+    Tn, hq, d = q_new.shape
+    B, hkv, cap, _ = k_cache.shape
+    _need(q_new, "q_new", torch.bfloat16)
+    _need(k_new, "k_new", torch.bfloat16, (Tn, hkv, d))
+    _need(v_new, "v_new", torch.bfloat16, (Tn, hkv, d))
+    _need(k_cache, "k_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(v_cache, "v_cache", torch.bfloat16, (B, hkv, cap, d))
+    _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
+    _need(cu_seqlens_new, "cu_seqlens_new", torch.int32, (B + 1,))
+    _need(pos1_new, "pos1_new", torch.int32, (Tn,))
+    _need(pos2_new, "pos2_new", torch.int32, (Tn,))
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o = torch.empty_like(q_new)
+    lse = torch.empty((hq, Tn), dtype=torch.float32, device=q_new.device) \
+        if return_lse else None
+    _check(lib().ism_attn_prefill_cached_rope2d(
+        _ptr(cu_seqlens_new), B, Tn, int(max_new), int(bool(seg_is_query)),
+        _ptr(q_new), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap,
+        _ptr(cache_seqlens), _ptr(pos1_new), _ptr(pos2_new), float(base), _ptr(o),
+        _ptr(lse), hq, hkv, d, scale, None, 0, _stream()))
     return o, lse
 
 

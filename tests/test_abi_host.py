@@ -162,6 +162,33 @@ def test_cache_argument_errors(L):
                           None) == 1
 
 
+def test_rope_argument_errors(L):
+    # rotation: null tensor / positions, bad dtype, unsupported head dim, bad base
+    assert L.ism_rope2d(None, 0, 4, 1, 64, FAKE, FAKE, 10000.0, 0, None) == 1
+    assert L.ism_rope2d(FAKE, 0, 4, 1, 64, None, FAKE, 10000.0, 0, None) == 1
+    assert L.ism_rope2d(FAKE, 2, 4, 1, 64, FAKE, FAKE, 10000.0, 0, None) == 3
+    assert L.ism_rope2d(FAKE, 0, 4, 1, 96, FAKE, FAKE, 10000.0, 0, None) == 3
+    assert L.ism_rope2d(FAKE, 1, -1, 1, 64, FAKE, FAKE, 10000.0, 0, None) == 2
+    for base in (1.0, 0.5, float("inf"), float("nan")):
+        assert L.ism_rope2d(FAKE, 0, 4, 1, 64, FAKE, FAKE, base, 0, None) == 2
+    # positions: segments checked as for the forward
+    sg = _segs(FAKE, FAKE, FAKE, 2, 1, 10, 10)
+    assert L.ism_positions_2d(ctypes.byref(sg), FAKE, FAKE, None) == 2
+    sg = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
+    assert L.ism_positions_2d(ctypes.byref(sg), None, FAKE, None) == 1
+    # fused prefill: the prefill checks, then the positions and the base
+    assert L.ism_attn_prefill_cached_rope2d(
+        FAKE, 1, 10, 10, 1, FAKE, FAKE, FAKE, FAKE, FAKE, 8, FAKE, FAKE, FAKE, 10000.0,
+        FAKE, None, 1, 1, 64, 0.125, None, 0, None) == 6
+    assert L.ism_attn_prefill_cached_rope2d(
+        FAKE, 1, 10, 10, 1, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, None, FAKE, 10000.0,
+        FAKE, None, 1, 1, 64, 0.125, None, 0, None) == 1
+    assert L.ism_attn_prefill_cached_rope2d(
+        FAKE, 1, 10, 10, 0, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, FAKE, FAKE, 1.0,
+        FAKE, None, 1, 1, 64, 0.125, None, 0, None) == 2
+    assert L.ism_last_error()
+
+
 @pytest.mark.skipif(not NO_GPU, reason="only meaningful where no GPU exists")
 def test_no_device_is_reported(L):
     sg = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
