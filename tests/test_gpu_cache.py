@@ -178,6 +178,37 @@ def test_workload3_one_shot_rows():
         od[t], ld[t] = ops.decode(qd[t], kd[t], vd[t], Kc, Vc, pos, 0, w.scale)
         pos += 1
     torch.cuda.synchronize()
+    del Kc, Vc
+
+    # the same turn through a paged cache (pages of 256 scattered over a
+    # shuffled pool) gives the same bits
+    ps = 256
+    mp = w.cache_cap // ps
+    table = torch.from_numpy(np.random.default_rng(9).permutation(B * mp + 5)[:B * mp]
+                             .astype(np.int32).reshape(B, mp)).cuda()
+
+    def pool_of(c):
+        c = dev_bf16(c)
+        pool = torch.zeros((B * mp + 5, w.hkv, ps, w.d), dtype=c.dtype, device="cuda")
+        pool[table.view(-1).long()] = (c.view(B, w.hkv, mp, ps, w.d).permute(0, 2, 1, 3, 4)
+                                       .reshape(B * mp, w.hkv, ps, w.d))
+        return pool
+    Kp, Vp = pool_of(w.k_cache), pool_of(w.v_cache)
+    announce("workload 3 paged prefill and decode")
+    op, lp = ops.prefill_paged(dev_bf16(w.q_new), dev_bf16(w.k_new), dev_bf16(w.v_new), Kp, Vp,
+                               table, lens, torch.from_numpy(w.cu_new).cuda(),
+                               int(w.new_lens.max()), True, w.scale)
+    pos = lens + torch.from_numpy(w.new_lens).cuda()
+    same = True
+    for t in range(w.steps):
+        o_t, l_t = ops.decode_paged(qd[t], kd[t], vd[t], Kp, Vp, table, pos, 0, w.scale)
+        same &= bool(torch.equal(o_t.view(torch.int16), od[t].view(torch.int16)))
+        same &= bool(torch.equal(l_t, ld[t]))
+        pos += 1
+    torch.cuda.synchronize()
+    assert torch.equal(op.view(torch.int16), o.view(torch.int16)) and torch.equal(lp, lse)
+    assert same, "paged decode differs from the dense decode"
+    del Kp, Vp
     for b in (0, 13, 31):
         C, L, S = w.hist_len, int(w.new_lens[b]), w.steps
         dia = W.segments_from_lengths([
