@@ -192,6 +192,8 @@ def bench_cache(w, timer, reps, warmup):
                      "frac_peak_hbm": b_dec / ms_turn / 1e6 / PEAK_HBM_GBS,
                      "bytes": b_dec, "bytes_per_step": b_dec / w.steps,
                      "traffic_per_step": recorded_decode_traffic()}
+    out["read_ceiling"] = read_ceiling(timer)
+    out["decode"]["frac_of_read_ceiling"] = out["decode"]["gbs"] / out["read_ceiling"]["gbs"]
 
     # the same turn through a paged cache: pages of 256 positions scattered
     # over a shuffled pool, one block table row per dialogue
@@ -262,6 +264,36 @@ def bench_cache(w, timer, reps, warmup):
                              "rope_q_ms": ms_rq, "rope_q_gbs": rq_bytes / ms_rq / 1e6,
                              "rope_q_frac_peak_hbm": rq_bytes / ms_rq / 1e6 / PEAK_HBM_GBS}
     return out
+
+
+def read_ceiling(timer, nbytes=4 << 30):
+    """Streaming-read rate of a plain kernel (libism_calib.so): the practical
+    ceiling for the HBM-bound decode, reported beside the 8 TB/s spec.
+    Best of a few grid sizes over a 4 GiB buffer."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_2408_00539_amd", "libism_calib.so")
+    fn = ctypes.CDLL(path).ism_calib_stream_read
+    fn.restype = ctypes.c_int64
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                   ctypes.c_void_p]
+    buf = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    by_grid = {}
+    for grid in (1024, 2048, 4096, 8192):
+        def run():
+            n = fn(buf.data_ptr(), nbytes, out.data_ptr(), grid, stream)
+            if n < 0:
+                raise RuntimeError("stream-read launch failed")
+            return n
+        n = run()
+        ms = timer.run(run, 10, 2, WARM_MS / 4)
+        by_grid[grid] = n / ms / 1e6
+    best = max(by_grid.values())
+    del buf
+    return {"bytes": n, "gbs": best, "frac_peak_hbm": best / PEAK_HBM_GBS,
+            "gbs_by_grid": {str(g): round(v, 1) for g, v in by_grid.items()}}
 
 
 def bench_expansion(w, timer, reps, warmup, ism_step_ms):

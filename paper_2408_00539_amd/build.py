@@ -1,4 +1,5 @@
-"""Build libism_attn.so for gfx950 with hipcc (in-tree, no JIT cache).
+"""Build libism_attn.so for gfx950 with hipcc (in-tree, no JIT cache), and
+libism_calib.so, the benchmark's streaming-read helper (calib/).
 
 Usage: python -m paper_2408_00539_amd.build [--jobs N]
 Every call recompiles all sources; objects go to _build/ next to this file.
@@ -18,6 +19,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libism_attn.so")
+CALIB_SRC = os.path.join(HERE, "calib")
+CALIB_LIB = os.path.join(HERE, "libism_calib.so")
 ARCH = "gfx950"
 
 HIP_FLAGS = [
@@ -68,7 +71,17 @@ def build(jobs=None, verbose=False):
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB} from {len(srcs)} sources")
+    _link(CALIB_LIB, [_compile(src) for src in sorted(glob.glob(os.path.join(CALIB_SRC, "*.hip")))])
     return LIB
+
+
+def _link(lib, objs):
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}{r.stderr}")
+    os.replace(tmp, lib)
 
 
 def main(argv=None):
