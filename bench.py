@@ -511,6 +511,7 @@ def _short_kernel(name):
         t = re.match(r"ILi(\d+)E", rest[len(m.group(1)) + n:])
         return base + (f"<{t.group(1)}>" if t else "")
     name = name.replace("void ", "").replace("ism::(anonymous namespace)::", "")
+    name = name.replace("(anonymous namespace)::", "")
     return name.replace("ism::", "").split("(")[0]
 
 
