@@ -95,8 +95,9 @@ ism_status ism_attn_fwd(const ism_segments *sg, const void *q, const void *k,
 /* Backward of ism_attn_fwd (training on whole dialogues in one pass,
  * Sec. 1 and Sec. 3.3). Inputs q, k, v, o, dout bf16 and lse fp32 as written
  * by ism_attn_fwd on the same inputs. Outputs dq [T, hq, d], dk and dv
- * [T, hkv, d] in fp32, overwritten. `deterministic` != 0 selects the
- * reduction order that is bitwise repeatable from run to run.
+ * [T, hkv, d] in fp32, overwritten. Every reduction is bitwise repeatable
+ * from run to run (no atomics); `deterministic` is accepted for callers
+ * that request that and does not change the result.
  * Workspace: ISM_OP_BWD. */
 ism_status ism_attn_bwd(const ism_segments *sg, const void *q, const void *k,
                         const void *v, const void *o, const float *lse,
