@@ -8,10 +8,12 @@ A step is one training pass of the attention hot path over one batch of
 workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
 visibility prep, the forward and the backward. ``value`` is the
 useful (unmasked) TFLOP/s of that step: 4*d FLOPs per visible (row, key) pair
-and query head for the forward, 10*d for the backward. The other paths of the
-hot path are measured on their own workloads and reported under ``paths``:
-the grouped-KV forward (workload 2), the cached prefill and the decode stream
-(workload 3), the backward (workload 4).
+and query head for the forward, 10*d for the backward; ``tokens_per_s`` gives
+the same step as packed tokens per second. The other paths of the hot path
+are measured on their own workloads and reported under ``paths``: the
+grouped-KV forward (workload 2), the cached prefill and the decode stream
+(workload 3, dense and paged, with draft verification, 2-D positions and the
+measured streaming-read ceiling), the backward (workload 4).
 
 Two comparisons from the paper ride along under ``paths``: the training cost
 of the prefix mask's sample expansion against ISM's single pass over the same
@@ -126,27 +128,29 @@ def bench_training(w, timer, steps, warmup, with_bwd):
     f_fwd = 4 * w.d * w.hq * pairs
     f_bwd = 10 * w.d * w.hq * pairs
     res = {"visible_pairs_per_head": pairs}
+    T = int(w.segs.total)
     o, lse = ops.fwd(q, k, v, segs, w.scale)
     ms_fwd = timer.run(lambda: ops.fwd(q, k, v, segs, w.scale), steps, warmup,
                        WARM_MS)
     res["fwd"] = {"ms": ms_fwd, "tflops": f_fwd / ms_fwd / 1e9,
                   "frac_peak": f_fwd / ms_fwd / 1e9 / PEAK_BF16_TFLOPS,
-                  "flop": f_fwd}
+                  "flop": f_fwd, "tokens_per_s": T / ms_fwd * 1e3}
     if with_bwd:
         do = dev(w.do) if w.do is not None else torch.randn_like(q)
         ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale),
                            steps, warmup, WARM_MS)
         res["bwd"] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
                       "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
-                      "flop": f_bwd}
+                      "flop": f_bwd, "tokens_per_s": T / ms_bwd * 1e3}
 
         def step():
             o2, l2 = ops.fwd(q, k, v, segs, w.scale)
             ops.bwd(q, k, v, o2, l2, do, segs, w.scale)
         ms_step = timer.run(step, steps, warmup)
-        res["step"] = {"ms": ms_step, "flop": f_fwd + f_bwd}
+        res["step"] = {"ms": ms_step, "flop": f_fwd + f_bwd,
+                       "tokens_per_s": T / ms_step * 1e3}
     else:
-        res["step"] = {"ms": ms_fwd, "flop": f_fwd}
+        res["step"] = {"ms": ms_fwd, "flop": f_fwd, "tokens_per_s": T / ms_fwd * 1e3}
     return res
 
 
@@ -169,7 +173,8 @@ def bench_cache(w, timer, reps, warmup):
         "frac_peak_mfma": f_pf / ms_pf / 1e9 / PEAK_BF16_TFLOPS,
         "kv_gbs": b_pf / ms_pf / 1e6,
         "bound_ms": max(f_pf / PEAK_BF16_TFLOPS / 1e9, b_pf / PEAK_HBM_GBS / 1e6),
-        "flop": f_pf, "kv_bytes": b_pf}}
+        "flop": f_pf, "kv_bytes": b_pf,
+        "new_tokens_per_s": float(np.sum(L)) / ms_pf * 1e3}}
     out["prefill_cached"]["frac_of_bound"] = out["prefill_cached"]["bound_ms"] / ms_pf
 
     qd, kd, vd = dev(w.q_dec), dev(w.k_dec), dev(w.v_dec)
@@ -191,6 +196,7 @@ def bench_cache(w, timer, reps, warmup):
                      "gbs": b_dec / ms_turn / 1e6,
                      "frac_peak_hbm": b_dec / ms_turn / 1e6 / PEAK_HBM_GBS,
                      "bytes": b_dec, "bytes_per_step": b_dec / w.steps,
+                     "tokens_per_s": B * w.steps / ms_turn * 1e3,
                      "traffic_per_step": recorded_decode_traffic()}
     out["read_ceiling"] = read_ceiling(timer)
     out["decode"]["frac_of_read_ceiling"] = out["decode"]["gbs"] / out["read_ceiling"]["gbs"]
@@ -705,6 +711,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(step_ms, 4),
+        "tokens_per_s": round(tr["step"]["tokens_per_s"], 1),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
