@@ -6,7 +6,9 @@
 //     key i: the start of i's segment if it is a query segment, else i itself
 //     (every later row of the dialogue sees i as well, since lim is
 //     non-decreasing inside a dialogue and lim(j) >= j).
-//  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji).
+//  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji),
+//     stored negated so that the dK/dV kernel starts its dP accumulators at
+//     -delta and forms dS = P o dP' without a subtraction.
 //  3. dK/dV kernel, key-tile outer: a workgroup owns 128 keys of one KV head
 //     (32 per wave pair, lane <-> key), walks the query heads of the group
 //     and the 64-row tiles from seer[first key] to the dialogue end, and
@@ -51,7 +53,7 @@ bwd_prep_kernel(const int32_t *__restrict__ cu_segs,
   seer[j] = q ? cu_segs[lo] : j;
 }
 
-// delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads; also the
+// -delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads; also the
 // LSE in log2 units (lse * log2 e) that the dK/dV kernel stages per tile.
 template <int D>
 __global__ void __launch_bounds__(256)
@@ -76,7 +78,7 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
   for (int s = 1; s < LPR; s <<= 1) acc += __shfl_xor(acc, s);
   if (c == 0 && gid / LPR < pairs) {
     const int64_t row = rh / hq, h = rh % hq;
-    delta[h * total + row] = acc;
+    delta[h * total + row] = -acc;
     lse2[h * total + row] = lse[h * total + row] * kLog2e;
   }
 }
@@ -221,11 +223,12 @@ dkv_kernel(BwdArgs a, int ktiles) {
   bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
   // dS wave, one product stream per step: for the previous tile (stage sp,
-  // also its P buffer) dS = P o (dP - delta) in 16-row slices, each slice's
+  // also its P buffer) dS = P o dP' in 16-row slices, each slice's
   // dK^T[d][key] += Q^T[d][row] dS[row][key] products running beside the
-  // elementwise work of the next slice; then (DP) dP[row][key] = dO V^T of
-  // the current tile (stage st). The empty asm statements keep each slot's
-  // vector work in its slot (IR passes would otherwise sink it to its use).
+  // elementwise work of the next slice; then (DP) dP'[row][key] = dO V^T -
+  // delta of the current tile (stage st), the accumulators starting at the
+  // staged -delta. The empty asm statements keep each slot's vector work in
+  // its slot (IR passes would otherwise sink it to its use).
   auto ds_dp = [&](int sp, int st, auto has_ds, auto has_dp) __attribute__((always_inline)) {
     constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
     constexpr int NK = DS ? NKK * NDB : 0, N = NK + (DP ? NKS * NRB : 0);
@@ -233,23 +236,28 @@ dkv_kernel(BwdArgs a, int ktiles) {
     const char *dl = (const char *)sm.dout[st];
     const u32x4 *pp = sm.p[sp][pair];
     u32x4 pw[NKK];
-    f32x4 dlt[NRB][4];
+    f32x16 nd[NRB];  // -delta of the current tile's rows, as dP' accumulators
     if constexpr (DS) {
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) pw[kk] = pp[kk * 64 + lane];
+    }
+    if constexpr (DP) {
 #pragma unroll
       for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          dlt[rb][i] = *(const f32x4 *)&sm.delta[sp][32 * rb + 8 * i + 4 * hf];
+        for (int i = 0; i < 4; ++i) {
+          const f32x4 v = *(const f32x4 *)&sm.delta[st][32 * rb + 8 * i + 4 * hf];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) nd[rb][4 * i + j] = v[j];
+        }
     }
     u32x4 fw[NKK];
     // dS elements 2u, 2u + 1 of slice kk (accumulator elements 8 bt + 2u ..)
     auto ds_pair = [&](int kk, int u) __attribute__((always_inline)) {
       const int rb = kk >> 1, e0 = 8 * (kk & 1) + 2 * u;
       f32x2 x;
-      x[0] = bf16_lo(pw[kk][u]) * (dp[rb][e0] - dlt[rb][e0 >> 2][e0 & 3]);
-      x[1] = bf16_hi(pw[kk][u]) * (dp[rb][e0 + 1] - dlt[rb][e0 >> 2][(e0 & 3) + 1]);
+      x[0] = bf16_lo(pw[kk][u]) * dp[rb][e0];
+      x[1] = bf16_hi(pw[kk][u]) * dp[rb][e0 + 1];
       uint32_t w = cvt_bf16x2(x);
       asm volatile("" : "+v"(w));
       fw[kk][u] = w;
@@ -271,7 +279,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
       } else {
         constexpr int j = n - NK, ks = j / NRB, rb = j % NRB;
-        dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : dp[rb]);
+        dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? nd[rb] : dp[rb]);
       }
     };
     auto pre = [&](auto nc) __attribute__((always_inline)) {
@@ -378,9 +386,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
 
   using T_ = std::true_type;
   using F_ = std::false_type;
-  // The dS waves' first step reads the last stage's Q, P buffer and delta
-  // before any tile has filled them (and multiplies them by zeros): clear
-  // them. The first tile's transfer goes to stage 0 and is not touched.
+  // The dS waves' first step reads the last stage's Q and P buffer before
+  // any tile has filled them (and multiplies them by zeros): clear them. The
+  // first tile's transfer goes to stage 0 and is not touched.
   {
     constexpr int L = kDkvStages - 1;
     u32x4 *qz = (u32x4 *)sm.q[L];
@@ -389,7 +397,6 @@ dkv_kernel(BwdArgs a, int ktiles) {
     for (int i = tid; i < kBR * D / 8; i += 512) qz[i] = u32x4{};
 #pragma unroll
     for (int i = tid; i < 4 * 4 * 64; i += 512) pz[i] = u32x4{};
-    if (tid < kBR) sm.delta[L][tid] = 0.f;
   }
   // Start of step it (row tile rt): wait for its tile and synchronize; the
   // transfer of the next tile starts a few products into the step's product
@@ -524,7 +531,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
   const int rc = min(wq0 + l32, e - 1);
   const int lim_r = a.lim[rc];
   const float lse2 = a.lse2[(int64_t)head * a.total + rc];
-  const float dlt = a.delta[(int64_t)head * a.total + rc];
+  const float ndlt = a.delta[(int64_t)head * a.total + rc];  // -delta
   bf16x8 qf[NKS], df[NKS];
   {
     const bf16_t *qp = (const bf16_t *)a.q + ((int64_t)rc * a.hq + head) * D + hf * 8;
@@ -618,8 +625,8 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       };
       auto ds2 = [&](int kb, int r) __attribute__((always_inline)) {  // elements r, r + 1 (r even)
         f32x2 x;
-        x[0] = sc[kb][r] * (pc[kb][r] - dlt);
-        x[1] = sc[kb][r + 1] * (pc[kb][r + 1] - dlt);
+        x[0] = sc[kb][r] * (pc[kb][r] + ndlt);
+        x[1] = sc[kb][r + 1] * (pc[kb][r + 1] + ndlt);
         uint32_t w = cvt_bf16x2(x);
         asm volatile("" : "+v"(w));
         ds[kb][r >> 3][(r & 7) >> 1] = w;

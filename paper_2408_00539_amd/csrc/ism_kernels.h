@@ -117,7 +117,7 @@ struct BwdArgs {
   const void *q, *k, *v, *o, *dout;
   const float *lse;
   float *dq, *dk, *dv;
-  float *delta;             // [hq, T] workspace: rowsum(dO * O)
+  float *delta;             // [hq, T] workspace: -rowsum(dO * O)
   float *lse2;              // [hq, T] workspace: lse * log2(e)
   const int32_t *cu_seqlens;
   const int32_t *cu_segs;
