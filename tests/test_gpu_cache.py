@@ -34,7 +34,7 @@ def _setup(rng, hist, new, hq, hkv, d, cap):
 
 
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("hq,hkv", [(2, 2), (8, 2), (4, 1)])
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (8, 2), (4, 1), (8, 1)])
 def test_prefill_then_decode_small(d, hq, hkv):
     torch = torch_cuda()
     from paper_2408_00539_amd import ops
