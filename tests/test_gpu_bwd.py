@@ -45,7 +45,7 @@ LAYOUTS = {
 
 @pytest.mark.parametrize("layout", sorted(LAYOUTS))
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("hq,hkv", [(1, 1), (4, 1), (4, 4), (8, 2)])
+@pytest.mark.parametrize("hq,hkv", [(1, 1), (4, 1), (4, 4), (8, 2), (4, 2), (6, 2)])
 def test_small_shapes(layout, d, hq, hkv):
     segs = W.segments_from_lengths(LAYOUTS[layout])
     rng = np.random.default_rng(zlib.crc32(f"bwd/{layout}/{d}/{hq}/{hkv}".encode()))

@@ -72,7 +72,7 @@ def test_small_shapes(layout, d, hq, hkv):
     compare("LSE", lse, rl)
 
 
-@pytest.mark.parametrize("hq,hkv", [(6, 2), (3, 3), (16, 2)])
+@pytest.mark.parametrize("hq,hkv", [(6, 2), (3, 3), (16, 2), (4, 2), (12, 2)])
 def test_other_head_groups(hq, hkv):
     segs = W.segments_from_lengths([W.alternating([40, 90, 33, 70])])
     rng = np.random.default_rng(hq * 31 + hkv)
