@@ -86,7 +86,10 @@ class PageAllocator:
 
 class PagedKVCache:
     """Device page pools, one block table row per dialogue slot, and the turn
-    operations above. Pools are ``[num_pages, hkv, page_size, d]`` bf16."""
+    operations above. Pools are ``[num_pages, hkv, page_size, d]`` bf16. Each
+    call uploads the block table rows and lengths of its slots (a small
+    synchronous host-to-device copy): a reference loop, not a graph-captured
+    one."""
 
     def __init__(self, num_pages, page_size, slots, max_pages, hkv, d, device="cuda"):
         import torch
@@ -100,6 +103,21 @@ class PagedKVCache:
     @property
     def lens(self):
         return self.alloc.lens
+
+    def _reserve_all(self, slots, lengths):
+        """Reserve pages for every slot or, if one request fails, for none
+        (the pages reserved by this call go back to the pool)."""
+        if len(set(slots)) != len(slots):
+            raise ValueError("a slot appears twice in one call")
+        done = []
+        try:
+            for s, n in zip(slots, lengths):
+                self.alloc.reserve(s, n)
+                done.append(s)
+        except Exception:
+            for s in done:
+                self.alloc.rollback(s, int(self.alloc.lens[s]))
+            raise
 
     def _views(self, slots):
         import torch
@@ -115,8 +133,7 @@ class PagedKVCache:
         new_lens = [int(n) for n in new_lens]
         if len(new_lens) != len(slots) or min(new_lens, default=1) < 1:
             raise ValueError("one new length >= 1 per slot")
-        for s, n in zip(slots, new_lens):
-            self.alloc.reserve(s, self.alloc.lens[s] + n)
+        self._reserve_all(slots, [self.alloc.lens[s] + n for s, n in zip(slots, new_lens)])
         tab, lens = self._views(slots)
         cu = torch.tensor(np.concatenate([[0], np.cumsum(new_lens)]), dtype=torch.int32,
                           device=self.device)
@@ -130,8 +147,7 @@ class PagedKVCache:
         """One answer token for each slot in ``slots``. Returns (o, lse)."""
         import torch
         slots = list(slots)
-        for s in slots:
-            self.alloc.reserve(s, self.alloc.lens[s] + 1)
+        self._reserve_all(slots, [self.alloc.lens[s] + 1 for s in slots])
         tab, lens = self._views(slots)
         need = ops.workspace_size(ops.ISM_OP_DECODE, len(slots), 0, self.alloc.capacity,
                                   q.shape[1], self.hkv, self.d, num_splits)

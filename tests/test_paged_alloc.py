@@ -90,3 +90,20 @@ def test_random_churn_keeps_invariants():
         except (PoolExhausted, ValueError):
             pass
         _check_invariants(a)
+
+
+def test_cache_reservation_is_all_or_nothing():
+    """PagedKVCache reserves the pages of all its slots or of none (no GPU:
+    only the host bookkeeping runs before the launch)."""
+    from paper_2408_00539_amd.paged import PagedKVCache
+    cache = PagedKVCache.__new__(PagedKVCache)
+    cache.alloc = PageAllocator(num_pages=4, page_size=64, slots=3, max_pages=4)
+    cache.alloc.reserve(2, 128)
+    cache.alloc.lens[2] = 128
+    free_before = cache.alloc.free_pages()
+    with pytest.raises(PoolExhausted):
+        cache._reserve_all([0, 1], [64, 129])   # 1 page, then 3: only 2 are free
+    assert cache.alloc.held[0] == [] and cache.alloc.held[1] == []
+    assert cache.alloc.free_pages() == free_before
+    with pytest.raises(ValueError):
+        cache._reserve_all([0, 0], [1, 1])
