@@ -198,6 +198,20 @@ def bench_cache(w, timer, reps, warmup):
                      "bytes": b_dec, "bytes_per_step": b_dec / w.steps,
                      "tokens_per_s": B * w.steps / ms_turn * 1e3,
                      "traffic_per_step": recorded_decode_traffic()}
+    # per-step spread: one more turn with an event pair around every step
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(w.steps)]
+    pos = pos0.clone()
+    for t in range(w.steps):
+        ev[t][0].record()
+        ops.decode(qd[t], kd[t], vd[t], Kc, Vc, pos, 0, w.scale, workspace=ws)
+        ev[t][1].record()
+        pos += 1
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in ev)
+    out["decode"]["step_ms_min"] = per[0]
+    out["decode"]["step_ms_median"] = per[len(per) // 2]
+    out["decode"]["step_ms_max"] = per[-1]
     out["read_ceiling"] = read_ceiling(timer)
     out["decode"]["frac_of_read_ceiling"] = out["decode"]["gbs"] / out["read_ceiling"]["gbs"]
 
