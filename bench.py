@@ -118,6 +118,34 @@ class Timer:
         return self.a.elapsed_time(self.b) / reps
 
 
+def device_info():
+    """Name, compute units and maximum engine clock of the gfx950 agent, as
+    rocminfo reports them (run as a child process; None if unavailable)."""
+    import subprocess
+    exe = "/opt/rocm/bin/rocminfo"
+    try:
+        out = subprocess.run([exe], capture_output=True, text=True, timeout=30).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    for agent in out.split("Agent ")[1:]:
+        if "gfx950" not in agent:
+            continue
+        info = {}
+        for line in agent.splitlines():
+            key, _, val = line.strip().partition(":")
+            val = val.strip()
+            if key == "Name" and "arch" not in info:
+                info["arch"] = val
+            elif key == "Marketing Name" and val and "name" not in info:
+                info["name"] = val
+            elif key == "Compute Unit" and "compute_units" not in info:
+                info["compute_units"] = int(val)
+            elif key == "Max Clock Freq. (MHz)" and "max_clock_mhz" not in info:
+                info["max_clock_mhz"] = int(val)
+        return info
+    return None
+
+
 def bench_training(w, timer, steps, warmup, with_bwd):
     from paper_2408_00539_amd import ops
     import torch
@@ -742,6 +770,7 @@ def main():
                      "frac": round(dom["tflops"] / PEAK_BF16_TFLOPS, 4),
                      "traffic": recorded_traffic() if with_bwd else None},
         "cpu_baseline": cpu,
+        "device": device_info(),
         "paths": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                       for kk, vv in v.items()} for k, v in paths.items()},
     }
