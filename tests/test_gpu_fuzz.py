@@ -52,3 +52,66 @@ def test_generated_layouts(dialogues, hh, d, seed):
     compare("dQ", host_f64(dq), rq)
     compare("dK", host_f64(dk), rk)
     compare("dV", host_f64(dv), rv)
+
+
+hist_len = st.one_of(st.sampled_from([0, 1, 63, 64, 65, 127, 128, 129, 255, 256, 257]),
+                     st.integers(0, 400))
+new_len = st.one_of(st.sampled_from([1, 2, 31, 32, 33, 63, 64, 65]), st.integers(1, 150))
+
+
+@settings(max_examples=40, deadline=None, derandomize=True, database=None)
+@given(turns=st.lists(st.tuples(hist_len, new_len), min_size=1, max_size=4),
+       is_query=st.booleans(), hh=heads, d=st.sampled_from([64, 128]),
+       splits=st.sampled_from([0, 1, 3, 64]), seed=st.integers(0, 2 ** 31 - 1))
+def test_generated_cache_turns(turns, is_query, hh, d, splits, seed):
+    """Cached prefill of a query or answer segment over generated histories,
+    then two decode steps, against the oracle's stepwise path (Sec. 2.3)."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    hq, hkv = hh
+    rng = np.random.default_rng(seed)
+
+    def bits(*shape):
+        return W.to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    hist = [h for h, _ in turns]
+    new = [n for _, n in turns]
+    B, cap = len(turns), 640
+    kc = np.zeros((B, hkv, cap, d), np.uint16)
+    vc = np.zeros((B, hkv, cap, d), np.uint16)
+    for b, C in enumerate(hist):
+        kc[b, :, :C] = bits(hkv, C, d)
+        vc[b, :, :C] = bits(hkv, C, d)
+    cu = np.concatenate([[0], np.cumsum(new)]).astype(np.int32)
+    Tn = int(cu[-1])
+    qn, kn, vn = bits(Tn, hq, d), bits(Tn, hkv, d), bits(Tn, hkv, d)
+    scale = 1 / np.sqrt(d)
+    announce("fuzz cache", turns, is_query, hq, hkv, d, splits, seed)
+    Kc, Vc = dev_bf16(kc), dev_bf16(vc)
+    lens = torch.tensor(hist, dtype=torch.int32, device="cuda")
+    o, lse = ops.prefill_cached_segment(dev_bf16(qn), dev_bf16(kn), dev_bf16(vn), Kc, Vc, lens,
+                                        torch.from_numpy(cu).cuda(), max(new), is_query, scale)
+    torch.cuda.synchronize()
+    o, lse = host_f64(o), host_f64(lse)
+    kref, vref = [], []
+    for b, C in enumerate(hist):
+        r0, r1 = cu[b], cu[b + 1]
+        ro, rl, kk, vv = oracle.prefill_cached(
+            f64(kc[b, :, :C]).transpose(1, 0, 2), f64(vc[b, :, :C]).transpose(1, 0, 2),
+            f64(qn[r0:r1]), f64(kn[r0:r1]), f64(vn[r0:r1]), scale, new_is_query=is_query)
+        compare(f"O prefill b{b}", o[r0:r1], ro)
+        compare(f"LSE prefill b{b}", lse[:, r0:r1], rl)
+        kref.append(kk)
+        vref.append(vv)
+    pos = torch.tensor([h + n for h, n in turns], dtype=torch.int32, device="cuda")
+    for t in range(2):
+        q, k, v = bits(B, hq, d), bits(B, hkv, d), bits(B, hkv, d)
+        od, ld = ops.decode(dev_bf16(q), dev_bf16(k), dev_bf16(v), Kc, Vc, pos, 0, scale,
+                            num_splits=splits)
+        torch.cuda.synchronize()
+        od, ld = host_f64(od), host_f64(ld)
+        for b in range(B):
+            ro, rl, kref[b], vref[b] = oracle.decode_step(kref[b], vref[b], f64(q[b]),
+                                                          f64(k[b]), f64(v[b]), scale)
+            compare(f"O decode t{t} b{b}", od[b], ro)
+            compare(f"LSE decode t{t} b{b}", ld[:, b], rl)
+        pos += 1
