@@ -115,3 +115,61 @@ def test_generated_cache_turns(turns, is_query, hh, d, splits, seed):
             compare(f"O decode t{t} b{b}", od[b], ro)
             compare(f"LSE decode t{t} b{b}", ld[:, b], rl)
         pos += 1
+
+
+@settings(max_examples=30, deadline=None, derandomize=True, database=None)
+@given(turns=st.lists(st.tuples(hist_len, new_len), min_size=1, max_size=4),
+       is_query=st.booleans(), hh=heads, d=st.sampled_from([64, 128]),
+       page_size=st.sampled_from([64, 128, 192, 256]), splits=st.sampled_from([0, 2, 7]),
+       seed=st.integers(0, 2 ** 31 - 1))
+def test_generated_paged_equals_dense(turns, is_query, hh, d, page_size, splits, seed):
+    """The paged entry points on a shuffled page pool give the dense entry
+    points' results bit for bit, for a segment prefill and two decode steps."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    hq, hkv = hh
+    rng = np.random.default_rng(seed)
+
+    def bits(*shape):
+        return W.to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    hist = [h for h, _ in turns]
+    new = [n for _, n in turns]
+    B = len(turns)
+    mp = -(-(max(h + n for h, n in turns) + 2) // page_size)
+    cap = mp * page_size
+    kc = np.zeros((B, hkv, cap, d), np.uint16)
+    vc = np.zeros((B, hkv, cap, d), np.uint16)
+    for b, C in enumerate(hist):
+        kc[b, :, :C] = bits(hkv, C, d)
+        vc[b, :, :C] = bits(hkv, C, d)
+    npages = B * mp + 3
+    table = rng.permutation(npages)[:B * mp].astype(np.int32).reshape(B, mp)
+
+    def pool_of(c):
+        pool = np.zeros((npages, hkv, page_size, d), np.uint16)
+        for b in range(B):
+            for j in range(mp):
+                pool[table[b, j]] = c[b, :, j * page_size:(j + 1) * page_size]
+        return dev_bf16(pool)
+    cu = torch.from_numpy(np.concatenate([[0], np.cumsum(new)]).astype(np.int32)).cuda()
+    Tn = sum(new)
+    qn, kn, vn = dev_bf16(bits(Tn, hq, d)), dev_bf16(bits(Tn, hkv, d)), dev_bf16(bits(Tn, hkv, d))
+    lens = torch.tensor(hist, dtype=torch.int32, device="cuda")
+    Kd, Vd, Kp, Vp = dev_bf16(kc), dev_bf16(vc), pool_of(kc), pool_of(vc)
+    tab = torch.from_numpy(table).cuda()
+    announce("fuzz paged", turns, is_query, hq, hkv, d, page_size, splits, seed)
+    od, ld = ops.prefill_cached_segment(qn, kn, vn, Kd, Vd, lens, cu, max(new), is_query)
+    op, lp = ops.prefill_paged(qn, kn, vn, Kp, Vp, tab, lens, cu, max(new), is_query)
+    outs = [(od, op), (ld, lp)]
+    pos = lens + torch.tensor(new, dtype=torch.int32, device="cuda")
+    for t in range(2):
+        q, k, v = dev_bf16(bits(B, hq, d)), dev_bf16(bits(B, hkv, d)), dev_bf16(bits(B, hkv, d))
+        outs.append(tuple(ops.decode(q, k, v, Kd, Vd, pos, 0, num_splits=splits)))
+        outs.append(tuple(ops.decode_paged(q, k, v, Kp, Vp, tab, pos, 0, num_splits=splits)))
+        pos += 1
+    torch.cuda.synchronize()
+    for a, b in outs[:2]:
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b)
+    for (oa, la), (ob, lb) in zip(outs[2::2], outs[3::2]):
+        assert torch.equal(oa.view(torch.int16), ob.view(torch.int16)) and torch.equal(la, lb)
