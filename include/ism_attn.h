@@ -92,6 +92,18 @@ ism_status ism_attn_fwd(const ism_segments *sg, const void *q, const void *k,
                         int32_t hkv, int32_t d, float scale, void *ws,
                         size_t ws_bytes, void *stream);
 
+/* Visibility metadata of a packed batch (Eq. 5, 0-indexed): lim[j] is the
+ * last key token j may see (the last token of j's segment if that is a query
+ * segment, j itself in an answer segment); seer[i] is the first token of
+ * i's dialogue that sees key i (the first token of i's segment if that is a
+ * query segment, i itself otherwise). Within a dialogue starting at s_b,
+ * token j sees key i iff s_b <= i <= lim[j], equivalently iff seer[i] <= j.
+ * These are the bounds from which the attention kernels classify their
+ * tiles (skipped, unmasked, masked). lim and seer [total_tokens] int32
+ * device, written. */
+ism_status ism_visibility(const ism_segments *sg, int32_t *lim, int32_t *seer,
+                          void *stream);
+
 /* Backward of ism_attn_fwd (training on whole dialogues in one pass,
  * Sec. 1 and Sec. 3.3). Inputs q, k, v, o, dout bf16 and lse fp32 as written
  * by ism_attn_fwd on the same inputs. Outputs dq [T, hq, d], dk and dv
@@ -116,8 +128,11 @@ ism_status ism_attn_bwd(const ism_segments *sg, const void *q, const void *k,
  * k_cache / v_cache [batch, hkv, cache_cap, d] bf16, updated in place only in
  * the append range; cache_seqlens [batch] device int32, read only (the
  * caller advances it by L_b afterwards). o [Tn, hq, d] bf16, lse [hq, Tn]
- * fp32 or NULL. The caller guarantees C_b + L_b <= cache_cap; max_new must
- * be >= every L_b. Workspace: ISM_OP_PREFILL_CACHED. */
+ * fp32 or NULL. The caller guarantees 0 <= C_b and C_b + L_b <= cache_cap
+ * (the lengths live on the device, so the call cannot check them): a
+ * dialogue outside that range gets NaN in all its rows of o and lse, and
+ * only its positions inside the cache are appended. max_new must be >= every
+ * L_b. Workspace: ISM_OP_PREFILL_CACHED (none). */
 ism_status ism_attn_prefill_cached(
     const int32_t *cu_seqlens_new, int32_t batch, int32_t total_new,
     int32_t max_new, const void *q_new, const void *k_new, const void *v_new,
@@ -149,11 +164,15 @@ ism_status ism_attn_prefill_cached_segment(
  * [0, p_b]. Each dialogue's key range is split into `num_splits` chunks of
  * equal length (0 = choose automatically), processed in parallel and merged
  * exactly. o [batch, hq, d]
- * bf16; lse [hq, batch] fp32 or NULL. The caller guarantees p_b < cache_cap
- * and advances cache_seqlens by 1 afterwards. max_seqlen bounds p_b + 1 for
- * the split choice (0 = cache_cap). Workspace: ism_attn_workspace_size(
- * ISM_OP_DECODE, batch, 0, max_seqlen (with 0 replaced by cache_cap), hq,
- * hkv, d, num_splits). */
+ * bf16; lse [hq, batch] fp32 or NULL. The caller guarantees
+ * 0 <= p_b < cache_cap and advances cache_seqlens by 1 afterwards; a
+ * dialogue with p_b outside that range gets NaN in o and lse and nothing is
+ * appended. max_seqlen bounds p_b + 1 for the split choice (0 = cache_cap):
+ * the split count, and with it the workspace size, has to be known on the
+ * host, where the positions (device memory) are not. Workspace:
+ * ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen (with 0
+ * replaced by cache_cap), hq, hkv, d, num_splits). Any hq / hkv is
+ * supported; a workgroup serves up to 8 query heads of one KV head. */
 ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            void *k_cache, void *v_cache, int32_t cache_cap,
                            const int32_t *cache_seqlens, int32_t batch,

@@ -25,5 +25,8 @@ from .ism_oracle import (  # noqa: F401
     decode_step,
     brute_force_fwd,
     visible_pairs,
+    seer,
+    uniform_fwd,
+    uniform_bwd,
 )
 from .rope2d import positions_2d, rope2d  # noqa: F401,E402

@@ -339,6 +339,92 @@ def decode_step(k_cache, v_cache, q, k, v, scale):
 
 
 # --------------------------------------------------------------------------
+# Who sees a key, and closed forms at Q = 0
+# --------------------------------------------------------------------------
+
+def seer(cu_seqlens, cu_segs, seg_is_query):
+    """First token of each key's dialogue that sees the key under Eq. 5:
+    seer(i) = min { j in i's dialogue : i <= lim(j) }.
+
+    lim is non-decreasing inside a dialogue (a query segment's tokens all map
+    to the segment end, which is below the next token; an answer token maps
+    to itself), so the minimum is the first j whose lim reaches i; the
+    monotonicity is asserted, not assumed.
+    """
+    L = lim(cu_seqlens, cu_segs, seg_is_query)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    out = np.empty_like(L)
+    for b in range(len(cu) - 1):
+        s, e = int(cu[b]), int(cu[b + 1])
+        Lb = L[s:e]
+        assert np.all(np.diff(Lb) >= 0), "lim must be non-decreasing in a dialogue"
+        out[s:e] = s + np.searchsorted(Lb, np.arange(s, e), side="left")
+    return out
+
+
+def _visible_counts(cu_seqlens, cu_segs, seg_is_query):
+    """n_j = lim(j) - s_b + 1 visible keys per token, and s_b per token."""
+    L = lim(cu_seqlens, cu_segs, seg_is_query)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    sb = cu[seq_index(cu_seqlens, len(L))]
+    return L - sb + 1, sb, L
+
+
+def _range_sums(x, sb, L):
+    """sum_{i = sb[j]}^{L[j]} x[i] for every j, through fp64 prefix sums."""
+    c = np.concatenate([np.zeros((1,) + x.shape[1:]), np.cumsum(x, axis=0)])
+    return c[L + 1] - c[sb]
+
+
+def uniform_fwd(v, cu_seqlens, cu_segs, seg_is_query):
+    """Forward at Q = 0 (any scale): every visible score is 0, so row j's
+    softmax weights are 1 / n_j on its n_j = lim(j) - s_b + 1 visible keys
+    (Eq. 5) and the outputs are O_j = mean(V[s_b .. lim(j)]),
+    LSE_j = ln n_j. v [T, Hkv, d]; returns (o [T, Hkv, d], lse [T]): query
+    head h takes o[:, h // (Hq / Hkv)], every head the same lse.
+    """
+    n, sb, L = _visible_counts(cu_seqlens, cu_segs, seg_is_query)
+    v = np.asarray(v, dtype=np.float64)
+    o = _range_sums(v, sb, L) / n[:, None, None]
+    return o, np.log(n.astype(np.float64))
+
+
+def uniform_bwd(k, v, hq, scale, cu_seqlens, cu_segs, seg_is_query,
+                row_weight=None):
+    """Gradients at Q = 0 and dO = 1 (all ones), from the chain rule of the
+    backward with P_ji = 1 / n_j on the visible keys:
+    dP_ji = dO_j . V_i = r_i (the row sum of V_i); D_j = mean of r over j's
+    keys; dS_ji = (r_i - D_j) / n_j; dQ_j = scale sum_i dS_ji K_i;
+    dK = scale dS^T Q = 0; dV_i = sum over the G query heads of kv head g and
+    the rows j that see i (seer(i) <= j < e_b) of P_ji.
+
+    ``row_weight`` [T] replaces the weight 1 / n_j in dV only (a test may
+    pass the weights rounded as a device rounds them). Returns
+    (dq [T, Hq, d], dk [T, Hkv, d], dv [T, Hkv, d]).
+    """
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    T, hkv, d = k.shape
+    G = _group(hq, hkv)
+    n, sb, L = _visible_counts(cu_seqlens, cu_segs, seg_is_query)
+    r = v.sum(axis=2)                                   # [T, hkv]
+    D = _range_sums(r, sb, L) / n[:, None]              # [T, hkv]
+    sum_rk = _range_sums(r[:, :, None] * k, sb, L)      # [T, hkv, d]
+    sum_k = _range_sums(k, sb, L)
+    dq_kv = scale * (sum_rk - D[:, :, None] * sum_k) / n[:, None, None]
+    dq = np.repeat(dq_kv, G, axis=1)
+    w = 1.0 / n if row_weight is None else np.asarray(row_weight, np.float64)
+    # dV_i = G * sum_{j = seer(i)}^{e_b - 1} w_j: suffix sums inside each dialogue
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    se = seer(cu_seqlens, cu_segs, seg_is_query)
+    eb = cu[seq_index(cu_seqlens, T) + 1]
+    c = np.concatenate([[0.0], np.cumsum(w)])
+    dv1 = G * (c[eb] - c[se])
+    dv = np.repeat(dv1[:, None, None], hkv, axis=1) * np.ones((1, 1, d))
+    return dq, np.zeros_like(k), dv
+
+
+# --------------------------------------------------------------------------
 # Brute force (tiny inputs): per-element loops of Eq. 4 with softmax
 # --------------------------------------------------------------------------
 

@@ -88,11 +88,13 @@ ism_status hip_status(hipError_t e, const char *what) {
   return fail(ISM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-int decode_splits(int32_t batch, int32_t hkv, int32_t max_len, int32_t req) {
+// Split count of a decode step; `sets` = head sets per dialogue (hkv when
+// hq / hkv <= 8).
+int decode_splits(int32_t batch, int32_t sets, int32_t max_len, int32_t req) {
   if (req > 0) return req;
   // about 2048 workgroups (two rounds of four per CU), at least 256 keys
   // per chunk, at most 64 chunks
-  const int slabs = batch * hkv;
+  const int slabs = batch * sets;
   int s = (2048 + slabs - 1) / slabs;
   const int by_len = (max_len + 255) / 256;
   if (s > by_len) s = by_len;
@@ -116,8 +118,9 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
     case ISM_OP_PREFILL_CACHED:
       return 0;
     case ISM_OP_DECODE: {
-      if (hkv < 1) return 0;
-      const size_t s = (size_t)decode_splits(batch, hkv, max_seqlen, num_splits);
+      if (hkv < 1 || hq < hkv || hq % hkv) return 0;
+      const int sets = hq / ism::decode_heads_per_set(hq, hkv);
+      const size_t s = (size_t)decode_splits(batch, sets, max_seqlen, num_splits);
       return align_up((size_t)batch * hq * s * d * 4) +
              align_up((size_t)batch * hq * s * 2 * 4);
     }
@@ -159,6 +162,18 @@ extern "C" ism_status ism_attn_fwd(const ism_segments *sg, const void *q,
   a.kv_row_stride = (int64_t)hkv * d;
   a.scale = scale;
   return hip_status(ism::launch_fwd(a, d, false, s), "forward launch");
+}
+
+extern "C" ism_status ism_visibility(const ism_segments *sg, int32_t *lim, int32_t *seer,
+                                     void *stream) {
+  ism::clear_error();
+  ism_status st = check_segments(sg);
+  if (st) return st;
+  if (!lim || !seer) return fail(ISM_ERR_NULL, "lim and seer are required");
+  if ((st = check_device())) return st;
+  return hip_status(ism::launch_bwd_prep(sg->cu_segs, sg->seg_is_query, sg->num_segs,
+                                         sg->total_tokens, lim, seer, (hipStream_t)stream),
+                    "visibility launch");
 }
 
 extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
@@ -408,16 +423,14 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
     return fail(ISM_ERR_SHAPE, "need batch >= 1 and cache_cap >= 1");
   ism_status st = check_heads(hq, hkv, d, scale);
   if (st) return st;
-  const int g = hq / hkv;
-  if (g != 1 && g != 2 && g != 4 && g != 8)
-    return fail(ISM_ERR_UNSUPPORTED, "decode supports hq/hkv in {1,2,4,8} (got %d)", g);
   if (max_seqlen == 0) max_seqlen = cache_cap;
   if (max_seqlen < 1 || max_seqlen > cache_cap)
     return fail(ISM_ERR_CAPACITY, "max_seqlen %d outside [1, cache_cap=%d]", max_seqlen,
                 cache_cap);
   if (num_splits < 0 || num_splits > 1024)
     return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
-  const int splits = decode_splits(batch, hkv, max_seqlen, num_splits);
+  const int splits =
+      decode_splits(batch, hq / ism::decode_heads_per_set(hq, hkv), max_seqlen, num_splits);
   const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen, hq,
                                               hkv, d, num_splits);
   if ((st = check_ws(ws, ws_bytes, need))) return st;
@@ -467,3 +480,4 @@ extern "C" ism_status ism_attn_decode_paged(const void *q, const void *k_new,
   return decode_impl(q, k_new, v_new, k_pages, v_pages, 0, cache_seqlens, batch, max_seqlen, o,
                      lse, hq, hkv, d, scale, num_splits, ws, ws_bytes, stream, &pg);
 }
+

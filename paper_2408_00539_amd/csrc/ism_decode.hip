@@ -70,22 +70,31 @@ cache_append_paged_kernel(const bf16_t *__restrict__ k_src, const bf16_t *__rest
 // PAGED: the cache is a page pool (DecodeArgs); the keys of one wave
 // iteration (KPW consecutive, KPW-aligned) lie in one page, whose address
 // is looked up once per iteration.
-template <int D, int G, bool PAGED>
+// A workgroup serves GS query heads that share one KV head (GS divides
+// G = hq / hkv and is at most 8, so that the per-head registers fit): head
+// set hs covers query heads hs GS .. hs GS + GS - 1 of KV head hs GS / G.
+// With G > 8 the G / GS sets of a KV head stream its keys separately.
+template <int D, int GS, bool PAGED>
 __global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
   constexpr int CPK = D / 8;     // lanes per key row (16 bytes each)
   constexpr int KPI = 64 / CPK;  // keys per wave-wide load
   constexpr int U = 8;           // loads in flight per lane per tensor
   constexpr int KPW = U * KPI;   // keys per wave per iteration
-  __shared__ float sm_o[4][G][D];
-  __shared__ float sm_m[4][G], sm_l[4][G];
+  __shared__ float sm_o[4][GS][D];
+  __shared__ float sm_m[4][GS], sm_l[4][GS];
 
-  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int split = blockIdx.x, hs = blockIdx.y, b = blockIdx.z;
+  const int head0 = hs * GS;
+  const int kvh = head0 / (a.hq / a.hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane % CPK, slot = lane / CPK;
-  // position of the new token; clamped so that out-of-contract positions
-  // never address memory outside the slab
-  const int p = min(max(a.pos[b], 0), a.cap - 1);
+  // position of the new token; an out-of-contract position (outside the
+  // cache) is clamped so that no access leaves the slab, nothing is
+  // appended, and the combine writes NaN for the dialogue
+  const int praw = a.pos[b];
+  const bool in_cap = praw >= 0 && praw < a.cap;
+  const int p = min(max(praw, 0), a.cap - 1);
   // chunk * splits >= p + 1, so the chunks cover [0, p] and p / chunk is a
   // valid split
   constexpr int kGran = 4 * KPW;
@@ -106,8 +115,9 @@ decode_split_kernel(DecodeArgs a) {
   const bf16_t *kn = (const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
   const bf16_t *vn = (const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + c * 8;
 
-  if (split == owner && tid < CPK) {
-    // this chunk owns the new token: store it into the cache
+  if (in_cap && split == owner && head0 % (a.hq / a.hkv) == 0 && tid < CPK) {
+    // this chunk (of the KV head's first head set) owns the new token:
+    // store it into the cache
     const int64_t prow = row_of(p);
     *(u32x4 *)((bf16_t *)a.k_cache + prow + tid * 8) =
         *(const u32x4 *)((const bf16_t *)a.k_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
@@ -115,20 +125,20 @@ decode_split_kernel(DecodeArgs a) {
         *(const u32x4 *)((const bf16_t *)a.v_new + ((int64_t)b * a.hkv + kvh) * D + tid * 8);
   }
 
-  float qv[G][8];
+  float qv[GS][8];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+  for (int g = 0; g < GS; ++g) {
     const u32x4 w = *(const u32x4 *)((const bf16_t *)a.q +
-                                     ((int64_t)b * a.hq + kvh * G + g) * D + c * 8);
+                                     ((int64_t)b * a.hq + head0 + g) * D + c * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       qv[g][2 * i] = bf16_lo(w[i]) * sl2;
       qv[g][2 * i + 1] = bf16_hi(w[i]) * sl2;
     }
   }
-  float m[G], l[G], o[G][8];
+  float m[GS], l[GS], o[GS][8];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+  for (int g = 0; g < GS; ++g) {
     m[g] = -INFINITY;
     l[g] = 0.f;
 #pragma unroll
@@ -152,7 +162,7 @@ decode_split_kernel(DecodeArgs a) {
       vr[u] = __builtin_nontemporal_load((const u32x4 *)(isnew ? vn : vc + (int64_t)key * D));
     }
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+    for (int g = 0; g < GS; ++g) {
       float s[U];
       float mt = -INFINITY;
 #pragma unroll
@@ -190,7 +200,7 @@ decode_split_kernel(DecodeArgs a) {
 
   // merge the key slots of the wave (lanes with equal c), then the 4 waves
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+  for (int g = 0; g < GS; ++g) {
 #pragma unroll
     for (int x = CPK; x < 64; x <<= 1) {
       const float m2 = __shfl_xor(m[g], x);
@@ -213,7 +223,7 @@ decode_split_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
-  for (int t = tid; t < G * D; t += 256) {
+  for (int t = tid; t < GS * D; t += 256) {
     const int g = t / D, dd = t % D;
     float mx = -INFINITY;
 #pragma unroll
@@ -226,7 +236,7 @@ decode_split_kernel(DecodeArgs a) {
       lt += sm_l[w][g] * f;
       ot += sm_o[w][g][dd] * f;
     }
-    const int h = kvh * G + g;
+    const int h = head0 + g;
     const int64_t pi = ((int64_t)b * a.hq + h) * a.splits + split;
     a.part_o[pi * D + dd] = ot;
     if (dd == 0) {
@@ -237,12 +247,21 @@ decode_split_kernel(DecodeArgs a) {
 }
 
 // Exact merge of the split partials: M = max m_s, L = sum l_s 2^(m_s - M),
-// O = sum o_s 2^(m_s - M) / L. Scores were kept in log2 units.
+// O = sum o_s 2^(m_s - M) / L. Scores were kept in log2 units. A dialogue
+// whose position lies outside the cache (out of contract) gets NaN.
 template <int D>
 __global__ void __launch_bounds__(D)
 decode_combine_kernel(DecodeArgs a) {
   const int bh = blockIdx.x;  // b * hq + h
   const int dd = threadIdx.x;
+  {
+    const int b = bh / a.hq, pb = a.pos[b];
+    if (pb < 0 || pb >= a.cap) {
+      ((bf16_t *)a.o)[(int64_t)bh * D + dd] = (bf16_t)NAN;
+      if (a.lse && dd == 0) a.lse[(int64_t)(bh % a.hq) * a.batch + b] = NAN;
+      return;
+    }
+  }
   const float *ml = a.part_ml + (int64_t)bh * a.splits * 2;
   float mx = -INFINITY;
   for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, ml[2 * s]);
@@ -261,14 +280,13 @@ decode_combine_kernel(DecodeArgs a) {
   }
 }
 
-template <int D, int G>
+template <int D, int GS>
 hipError_t launch_decode_t(const DecodeArgs &a, hipStream_t stream) {
+  const dim3 grid(a.splits, a.hq / GS, a.batch);
   if (a.block_table)
-    hipLaunchKernelGGL((decode_split_kernel<D, G, true>), dim3(a.splits, a.hkv, a.batch),
-                       dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, GS, true>), grid, dim3(256), 0, stream, a);
   else
-    hipLaunchKernelGGL((decode_split_kernel<D, G, false>), dim3(a.splits, a.hkv, a.batch),
-                       dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, GS, false>), grid, dim3(256), 0, stream, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(a.batch * a.hq), dim3(D),
@@ -278,10 +296,14 @@ hipError_t launch_decode_t(const DecodeArgs &a, hipStream_t stream) {
 
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
-  switch (a.hq / a.hkv) {
+  switch (decode_heads_per_set(a.hq, a.hkv)) {
     case 1: return launch_decode_t<D, 1>(a, stream);
     case 2: return launch_decode_t<D, 2>(a, stream);
+    case 3: return launch_decode_t<D, 3>(a, stream);
     case 4: return launch_decode_t<D, 4>(a, stream);
+    case 5: return launch_decode_t<D, 5>(a, stream);
+    case 6: return launch_decode_t<D, 6>(a, stream);
+    case 7: return launch_decode_t<D, 7>(a, stream);
     case 8: return launch_decode_t<D, 8>(a, stream);
     default: return hipErrorInvalidValue;
   }

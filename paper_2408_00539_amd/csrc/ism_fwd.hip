@@ -287,13 +287,16 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   const int wg_last = min(q0 + wg_rows, e) - 1;
 
   int key_begin, key_hi, wave_lo, wave_hi, cache_c = 0;
+  bool oob = false;  // cache mode: C_b + L_b outside the cache (out of contract)
   const bf16_t *kbase, *vbase;
   if (CACHE) {
     key_begin = 0;
     cache_c = a.cache_len[b];
     // keys [0, C_b + L_b) (query segment) or [0, C_b + r] for row r (answer
-    // segment); clamped to the slab for out-of-contract lengths
+    // segment); clamped to the slab for out-of-contract lengths, whose rows
+    // get NaN
     const int slab_rows = PAGED ? a.max_pages * a.page_size : (int)(a.kv_head_stride / D);
+    oob = cache_c < 0 || cache_c + (e - s) > slab_rows;
     if (a.cache_causal) {
       key_hi = max(min(cache_c + (wg_last - s) + 1, slab_rows) - 1, 0);
       wave_lo = min(cache_c + (min(wq0, e - 1) - s), key_hi);
@@ -467,7 +470,7 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
   const float lt = pair_sum(l_run);
   const int row = wq0 + l32;
   if (row >= e) return;
-  const float inv = 1.f / lt;
+  const float inv = oob ? __builtin_nanf("") : 1.f / lt;
   bf16_t *op = (bf16_t *)a.o + ((int64_t)row * a.hq + head) * D + hf * 4;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
@@ -478,7 +481,8 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
       w[1] = pack_bf16x2(oacc[db][4 * i + 2] * inv, oacc[db][4 * i + 3] * inv);
       *(u32x2 *)(op + db * 32 + 8 * i) = w;
     }
-  if (a.lse && hf == 0) a.lse[(int64_t)head * a.total_q + row] = m_run * a.scale + logf(lt);
+  if (a.lse && hf == 0)
+    a.lse[(int64_t)head * a.total_q + row] = oob ? __builtin_nanf("") : m_run * a.scale + logf(lt);
 }
 
 int gcd_int(int x, int y) {

@@ -113,6 +113,15 @@ struct DecodeArgs {
 
 hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream);
 
+// Query heads per decode workgroup: the largest divisor of G = hq / hkv
+// that is at most 8 (a workgroup keeps 8 + 10 registers per head).
+inline int decode_heads_per_set(int hq, int hkv) {
+  const int g = hq / hkv;
+  for (int s = 8; s > 1; --s)
+    if (g % s == 0) return s;
+  return 1;
+}
+
 struct BwdArgs {
   const void *q, *k, *v, *o, *dout;
   const float *lse;

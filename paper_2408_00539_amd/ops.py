@@ -6,9 +6,11 @@ stream to the C ABI, and raises on any status other than ISM_OK. There is no
 fallback: if the library is not built or no gfx950 device is present, the
 call fails loudly.
 
-Names follow the C ABI (include/ism_attn.h): fwd, bwd, prefill_cached,
-prefill_cached_segment, decode, prefill_paged, decode_paged, plus
-check_segments_host and workspace_size.
+Names follow the C ABI (include/ism_attn.h): fwd, bwd, visibility,
+prefill_cached, prefill_cached_segment, decode,
+prefill_paged, decode_paged, positions_2d, rope2d_, prefill_cached_rope2d,
+plus check_segments_host and workspace_size. Outputs are allocated with
+torch unless the caller passes them (``out=``).
 """
 
 from __future__ import annotations
@@ -69,6 +71,7 @@ _SIGS = {
                                    _Z, _P]),
     "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
                              _I, _I, _F, _I, _P, _Z, _P]),
+    "ism_visibility": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P]),
     "ism_positions_2d": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P]),
     "ism_rope2d": (_I, [_P, _I, _I, _I, _I, _P, _P, _F, _I, _P]),
     "ism_attn_prefill_cached_rope2d": (_I, [_P, _I, _I, _I, _I, _P, _P, _P,
@@ -141,6 +144,28 @@ def workspace_size(op, batch=0, total_tokens=0, max_seqlen=0, hq=0, hkv=0,
                                              num_splits))
 
 
+def _outputs(out, specs, device):
+    """Caller-provided outputs (checked) or new torch tensors.
+
+    specs: one (name, dtype, shape) per output; shape None = absent (the
+    caller's entry must then be None too)."""
+    torch = _torch()
+    if out is None:
+        return tuple(None if shp is None else
+                     torch.empty(shp, dtype=dt, device=device)
+                     for _, dt, shp in specs)
+    out = tuple(out)
+    if len(out) != len(specs):
+        raise ValueError(f"out must hold {len(specs)} tensors")
+    for t, (name, dt, shp) in zip(out, specs):
+        if shp is None:
+            if t is not None:
+                raise ValueError(f"{name} is not produced by this call")
+            continue
+        _need(t, name, dt, shp)
+    return out
+
+
 def _workspace(nbytes, device):
     torch = _torch()
     if nbytes == 0:
@@ -184,21 +209,24 @@ class Segments:
                             self.num_segs, self.total_tokens, self.max_seqlen)
 
 
-def fwd(q, k, v, segs, scale=None, return_lse=True):
+def fwd(q, k, v, segs, scale=None, return_lse=True, out=None):
     """ISM forward over packed dialogues. q [T,hq,d], k/v [T,hkv,d] bf16.
-    Returns (o bf16 [T,hq,d], lse fp32 [hq,T] or None)."""
+    Returns (o bf16 [T,hq,d], lse fp32 [hq,T] or None); ``out=(o, lse)``
+    writes into caller tensors instead."""
     torch = _torch()
-    T, hq, d = q.shape
-    hkv = k.shape[1]
     _need(q, "q", torch.bfloat16)
+    if q.dim() != 3:
+        raise ValueError("q must be [T, hq, d]")
+    T, hq, d = q.shape
+    hkv = k.shape[1] if k.dim() == 3 else -1
     _need(k, "k", torch.bfloat16, (T, hkv, d))
     _need(v, "v", torch.bfloat16, (T, hkv, d))
     if T != segs.total_tokens:
         raise ValueError("q rows != segs.total_tokens")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q)
-    lse = torch.empty((hq, T), dtype=torch.float32, device=q.device) \
-        if return_lse else None
+    o, lse = _outputs(out, [("o", torch.bfloat16, (T, hq, d)),
+                            ("lse", torch.float32,
+                             (hq, T) if return_lse else None)], q.device)
     nws = workspace_size(ISM_OP_FWD, segs.batch, T, segs.max_seqlen, hq, hkv, d)
     ws = _workspace(nws, q.device)
     sg = segs.c_struct()
@@ -208,18 +236,29 @@ def fwd(q, k, v, segs, scale=None, return_lse=True):
     return o, lse
 
 
-def bwd(q, k, v, o, lse, dout, segs, scale=None, deterministic=False):
-    """Gradients (dq [T,hq,d], dk, dv [T,hkv,d], fp32) of ism fwd."""
+def bwd(q, k, v, o, lse, dout, segs, scale=None, deterministic=False,
+        out=None):
+    """Gradients (dq [T,hq,d], dk, dv [T,hkv,d], fp32) of ism fwd;
+    ``out=(dq, dk, dv)`` writes into caller tensors instead.
+    ``deterministic`` selects the bitwise-repeatable path; the default
+    accumulates dQ with atomics in one pass (see ism_attn_bwd)."""
     torch = _torch()
+    _need(q, "q", torch.bfloat16)
+    if q.dim() != 3:
+        raise ValueError("q must be [T, hq, d]")
     T, hq, d = q.shape
-    hkv = k.shape[1]
-    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o"), (dout, "dout")):
-        _need(t, n, torch.bfloat16)
+    hkv = k.shape[1] if k.dim() == 3 else -1
+    _need(k, "k", torch.bfloat16, (T, hkv, d))
+    _need(v, "v", torch.bfloat16, (T, hkv, d))
+    _need(o, "o", torch.bfloat16, (T, hq, d))
+    _need(dout, "dout", torch.bfloat16, (T, hq, d))
     _need(lse, "lse", torch.float32, (hq, T))
+    if T != segs.total_tokens:
+        raise ValueError("q rows != segs.total_tokens")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    dq = torch.empty((T, hq, d), dtype=torch.float32, device=q.device)
-    dk = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
-    dv = torch.empty((T, hkv, d), dtype=torch.float32, device=q.device)
+    dq, dk, dv = _outputs(out, [("dq", torch.float32, (T, hq, d)),
+                                ("dk", torch.float32, (T, hkv, d)),
+                                ("dv", torch.float32, (T, hkv, d))], q.device)
     nws = workspace_size(ISM_OP_BWD, segs.batch, T, segs.max_seqlen, hq, hkv, d)
     ws = _workspace(nws, q.device)
     sg = segs.c_struct()
@@ -232,26 +271,32 @@ def bwd(q, k, v, o, lse, dout, segs, scale=None, deterministic=False):
 
 
 def prefill_cached(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
-                   cu_seqlens_new, max_new, scale=None, return_lse=True):
+                   cu_seqlens_new, max_new, scale=None, return_lse=True,
+                   out=None):
     """New query segment against the reused cache (appends k_new/v_new).
-    Returns (o [Tn,hq,d] bf16, lse [hq,Tn] fp32 or None)."""
+    Returns (o [Tn,hq,d] bf16, lse [hq,Tn] fp32 or None). A dialogue whose
+    C_b + L_b exceeds the cache gets NaN rows (the library cannot see the
+    device lengths before the launch)."""
     return _prefill(None, q_new, k_new, v_new, k_cache, v_cache,
-                    cache_seqlens, cu_seqlens_new, max_new, scale, return_lse)
+                    cache_seqlens, cu_seqlens_new, max_new, scale, return_lse,
+                    out)
 
 
 def prefill_cached_segment(q_new, k_new, v_new, k_cache, v_cache,
                            cache_seqlens, cu_seqlens_new, max_new,
-                           seg_is_query, scale=None, return_lse=True):
+                           seg_is_query, scale=None, return_lse=True,
+                           out=None):
     """New segment against the reused cache: a query segment (every new row
     sees the whole cache and all new rows) or, with seg_is_query false, an
     answer segment (new row r sees the cache and new rows 0..r)."""
     return _prefill(bool(seg_is_query), q_new, k_new, v_new, k_cache,
                     v_cache, cache_seqlens, cu_seqlens_new, max_new, scale,
-                    return_lse)
+                    return_lse, out)
 
 
 def _prefill(seg_is_query, q_new, k_new, v_new, k_cache, v_cache,
-             cache_seqlens, cu_seqlens_new, max_new, scale, return_lse):
+             cache_seqlens, cu_seqlens_new, max_new, scale, return_lse,
+             out=None):
     torch = _torch()
     Tn, hq, d = q_new.shape
     B, hkv, cap, _ = k_cache.shape
@@ -263,9 +308,9 @@ def _prefill(seg_is_query, q_new, k_new, v_new, k_cache, v_cache,
     _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
     _need(cu_seqlens_new, "cu_seqlens_new", torch.int32, (B + 1,))
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    o = torch.empty_like(q_new)
-    lse = torch.empty((hq, Tn), dtype=torch.float32, device=q_new.device) \
-        if return_lse else None
+    o, lse = _outputs(out, [("o", torch.bfloat16, (Tn, hq, d)),
+                            ("lse", torch.float32,
+                             (hq, Tn) if return_lse else None)], q_new.device)
     if seg_is_query is None:
         _check(lib().ism_attn_prefill_cached(
             _ptr(cu_seqlens_new), B, Tn, int(max_new), _ptr(q_new),
@@ -344,32 +389,58 @@ def prefill_cached_rope2d(q_new, k_new, v_new, k_cache, v_cache, cache_seqlens,
     return o, lse
 
 
-def decode(q, k_new, v_new, k_cache, v_cache, cache_seqlens, max_seqlen=0,
-           scale=None, num_splits=0, return_lse=True, workspace=None):
-    """One decode step (appends k_new/v_new at cache_seqlens[b]).
-    Returns (o [B,hq,d] bf16, lse [hq,B] fp32 or None)."""
+def _decode_args(q, k_new, v_new, k_cache, v_cache, cache_seqlens, scale,
+                 return_lse, out):
     torch = _torch()
+    _need(q, "q", torch.bfloat16)
+    if q.dim() != 3 or k_cache.dim() != 4:
+        raise ValueError("q must be [B, hq, d], k_cache [B, hkv, cap, d]")
     B, hq, d = q.shape
     _, hkv, cap, _ = k_cache.shape
-    _need(q, "q", torch.bfloat16)
     _need(k_new, "k_new", torch.bfloat16, (B, hkv, d))
     _need(v_new, "v_new", torch.bfloat16, (B, hkv, d))
     _need(k_cache, "k_cache", torch.bfloat16, (B, hkv, cap, d))
     _need(v_cache, "v_cache", torch.bfloat16, (B, hkv, cap, d))
     _need(cache_seqlens, "cache_seqlens", torch.int32, (B,))
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    o, lse = _outputs(out, [("o", torch.bfloat16, (B, hq, d)),
+                            ("lse", torch.float32,
+                             (hq, B) if return_lse else None)], q.device)
+    return B, hq, hkv, d, cap, scale, o, lse
+
+
+def decode(q, k_new, v_new, k_cache, v_cache, cache_seqlens, max_seqlen=0,
+           scale=None, num_splits=0, return_lse=True, workspace=None,
+           out=None):
+    """One decode step (appends k_new/v_new at cache_seqlens[b]).
+    Returns (o [B,hq,d] bf16, lse [hq,B] fp32 or None). A dialogue whose
+    position lies outside the cache gets NaN (nothing is appended)."""
+    B, hq, hkv, d, cap, scale, o, lse = _decode_args(
+        q, k_new, v_new, k_cache, v_cache, cache_seqlens, scale, return_lse,
+        out)
     ms = cap if not max_seqlen else int(max_seqlen)
     nws = workspace_size(ISM_OP_DECODE, B, 0, ms, hq, hkv, d, num_splits)
     ws = workspace if workspace is not None else _workspace(nws, q.device)
-    o = torch.empty_like(q)
-    lse = torch.empty((hq, B), dtype=torch.float32, device=q.device) \
-        if return_lse else None
     _check(lib().ism_attn_decode(
         _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap,
         _ptr(cache_seqlens), B, ms, _ptr(o), _ptr(lse), hq, hkv, d, scale,
         int(num_splits), _ptr(ws), nws if workspace is None else
         workspace.numel(), _stream()))
     return o, lse
+
+
+def visibility(segs):
+    """Eq. 5 visibility metadata as the kernels compute it: lim [T] (last
+    key each token sees) and seer [T] (first token that sees each key),
+    int32 on the GPU."""
+    torch = _torch()
+    dev = segs.cu_seqlens.device
+    lim_ = torch.empty(segs.total_tokens, dtype=torch.int32, device=dev)
+    seer = torch.empty_like(lim_)
+    st = segs.c_struct()
+    _check(lib().ism_visibility(ctypes.byref(st), _ptr(lim_), _ptr(seer),
+                                _stream()))
+    return lim_, seer
 
 
 def check_segments_host(cu_seqlens, cu_segs, seg_is_query, max_seqlen=None):

@@ -118,9 +118,12 @@ def test_fwd_argument_errors(L):
 
 def test_cache_argument_errors(L):
     ws = ctypes.c_void_p(FAKE * 256)
-    # decode: unsupported group size 3
+    # decode: query heads not a multiple of the KV heads
     assert L.ism_attn_decode(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1, 0, FAKE,
-                             None, 3, 1, 64, 0.125, 0, ws, 1 << 20, None) == 3
+                             None, 3, 2, 64, 0.125, 0, ws, 1 << 20, None) == 2
+    # visibility: outputs required
+    sgv = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
+    assert L.ism_visibility(ctypes.byref(sgv), None, FAKE, None) == 1
     # decode: max_seqlen beyond capacity
     assert L.ism_attn_decode(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1, 65, FAKE,
                              None, 1, 1, 64, 0.125, 0, ws, 1 << 20, None) == 6
@@ -205,6 +208,9 @@ def test_workspace_sizes(L):
     assert ops.workspace_size(ops.ISM_OP_PREFILL_CACHED, 1, 10, 10, 4, 4, 64) == 0
     a = ops.workspace_size(ops.ISM_OP_DECODE, 2, 0, 4096, 8, 2, 128, 4)
     assert a >= 2 * 8 * 4 * 128 * 4 + 2 * 8 * 4 * 2 * 4
+    # any head grouping has a decode workspace (groups above 8 run in sets)
+    for hq, hkv in ((3, 1), (12, 1), (32, 1), (6, 2)):
+        assert ops.workspace_size(ops.ISM_OP_DECODE, 2, 0, 4096, hq, hkv, 128) > 0
 
 
 def test_product_path_has_no_fallback():

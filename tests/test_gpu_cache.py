@@ -34,7 +34,8 @@ def _setup(rng, hist, new, hq, hkv, d, cap):
 
 
 @pytest.mark.parametrize("d", [64, 128])
-@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (8, 2), (4, 1), (8, 1)])
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (8, 2), (4, 1), (8, 1),
+                                    (3, 1), (12, 1), (16, 2), (6, 3)])
 def test_prefill_then_decode_small(d, hq, hkv):
     torch = torch_cuda()
     from paper_2408_00539_amd import ops
@@ -233,3 +234,55 @@ def test_workload3_one_shot_rows():
             compare(f"LSE prefill b{b} h{h}", host_f64(lse[h, r0:r1]), rl[:L])
             compare(f"O decode b{b} h{h}", host_f64(od[:, b, h]), ro[L:])
             compare(f"LSE decode b{b} h{h}", host_f64(ld[:, h, b]), rl[L:])
+
+
+def test_out_of_capacity_dialogues_get_nan():
+    """Out of contract (the lengths live on the device, so the host cannot
+    refuse them): a dialogue whose new segment would end past the cache, or
+    whose decode position lies outside it, gets NaN in all its rows and
+    nothing of it is written outside the cache; the other dialogues are
+    unaffected."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    rng = np.random.default_rng(31)
+    hq = hkv = 2
+    d, cap = 64, 256
+    hist, new = [10, 250, 100], [20, 20, 20]   # dialogue 1 ends at 270 > 256
+    kc, vc, cu_new, qn, kn, vn = _setup(rng, hist, new, hq, hkv, d, cap)
+    Kc, Vc = dev_bf16(kc), dev_bf16(vc)
+    announce("prefill out of capacity")
+    o, lse = ops.prefill_cached(dev_bf16(qn), dev_bf16(kn), dev_bf16(vn), Kc, Vc,
+                                torch.tensor(hist, dtype=torch.int32, device="cuda"),
+                                torch.from_numpy(cu_new).cuda(), max(new), 0.125)
+    torch.cuda.synchronize()
+    o, lse = host_f64(o), host_f64(lse)
+    assert np.all(np.isnan(o[cu_new[1]:cu_new[2]])) and np.all(np.isnan(lse[:, cu_new[1]:cu_new[2]]))
+    for b in (0, 2):
+        r0, r1 = cu_new[b], cu_new[b + 1]
+        C = hist[b]
+        ro, rl, _, _ = oracle.prefill_cached(
+            f64(kc[b, :, :C]).transpose(1, 0, 2), f64(vc[b, :, :C]).transpose(1, 0, 2),
+            f64(qn[r0:r1]), f64(kn[r0:r1]), f64(vn[r0:r1]), 0.125)
+        compare(f"O b{b}", o[r0:r1], ro)
+        compare(f"LSE b{b}", lse[:, r0:r1], rl)
+    Kh = Kc.view(torch.int16).cpu().numpy().view(np.uint16)
+    # dialogue 1: the six positions 250..255 inside the cache were appended
+    np.testing.assert_array_equal(Kh[1, :, 250:256],
+                                  kn[cu_new[1]:cu_new[1] + 6].transpose(1, 0, 2))
+    np.testing.assert_array_equal(Kh[1, :, :250], kc[1, :, :250])
+
+    # decode: positions cap (past the end) and -1 are out of contract
+    pos = torch.tensor([cap, 40, -1], dtype=torch.int32, device="cuda")
+    q, k, v = _bits(rng, 3, hq, d), _bits(rng, 3, hkv, d), _bits(rng, 3, hkv, d)
+    before = Kc.clone()
+    announce("decode out of capacity")
+    od, ld = ops.decode(dev_bf16(q), dev_bf16(k), dev_bf16(v), Kc, Vc, pos, 0, 0.125)
+    torch.cuda.synchronize()
+    od, ld = host_f64(od), host_f64(ld)
+    assert np.all(np.isnan(od[0])) and np.all(np.isnan(od[2]))
+    assert np.all(np.isnan(ld[:, 0])) and np.all(np.isnan(ld[:, 2]))
+    assert np.all(np.isfinite(od[1])) and np.all(np.isfinite(ld[:, 1]))
+    after = Kc.view(torch.int16).cpu().numpy()
+    bef = before.view(torch.int16).cpu().numpy()
+    np.testing.assert_array_equal(after[0], bef[0])
+    np.testing.assert_array_equal(after[2], bef[2])
