@@ -13,7 +13,8 @@
  * Conventions shared by every entry point:
  *  - Tensor pointers are DEVICE pointers owned by the caller. The library
  *    allocates no memory and keeps no state between calls other than a
- *    thread-local error string.
+ *    thread-local error string (and the fixed scratch array of
+ *    ism_attn_decode_noalloc, below).
  *  - bf16 tensors are passed as void* and are dense row-major:
  *      q, o: [T, hq, d];  k, v: [T, hkv, d]   (T = tokens of the packed batch)
  *      lse:  [hq, T] float32, natural-log log-sum-exp of the scaled scores.
@@ -180,6 +181,28 @@ ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            int32_t hkv, int32_t d, float scale,
                            int32_t num_splits, void *ws, size_t ws_bytes,
                            void *stream);
+
+/* The decode step of ism_attn_decode for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same arguments without the
+ * workspace. The split partials live in a fixed per-device scratch array of
+ * ISM_NOALLOC_SCRATCH_BYTES that the library holds until the process ends
+ * (its device address is looked up on the first call on each device); the
+ * call allocates nothing. Calls whose partials need more (batch * hq *
+ * splits * (d + 2) * 4 bytes, rounded up) fail with ISM_ERR_WORKSPACE
+ * before any launch. Every call on a device shares that device's scratch:
+ * calls that may overlap on one device (different streams, no ordering
+ * between them) race and must be serialised by the caller. Results equal
+ * those of ism_attn_decode bit for bit. */
+#define ISM_NOALLOC_SCRATCH_BYTES (8u << 20)
+ism_status ism_attn_decode_noalloc(const void *q, const void *k_new,
+                                   const void *v_new, void *k_cache,
+                                   void *v_cache, int32_t cache_cap,
+                                   const int32_t *cache_seqlens, int32_t batch,
+                                   int32_t max_seqlen, void *o, float *lse,
+                                   int32_t hq, int32_t hkv, int32_t d,
+                                   float scale, int32_t num_splits,
+                                   void *stream);
 
 /* Paged KV cache: the same two operations with the cache held in fixed-size
  * pages instead of one slab per dialogue, so that dialogues of very

@@ -4,6 +4,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/ism_attn.h"
 #include "ism_host.h"
 #include "ism_kernels.h"
@@ -481,3 +483,70 @@ extern "C" ism_status ism_attn_decode_paged(const void *q, const void *k_new,
                      lse, hq, hkv, d, scale, num_splits, ws, ws_bytes, stream, &pg);
 }
 
+// ---------------------------------------------------------------- no-allocation decode
+
+namespace {
+
+// Split partials of ism_attn_decode_noalloc: one array per device, held
+// until the process ends. Host code never passes this name to a kernel (on
+// the host it is only a stand-in for the device symbol): it uses the device
+// address that hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[ISM_NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[64];  // per device ordinal, set on the first call there
+
+ism_status scratch_address(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(ISM_ERR_NO_DEVICE, "hipGetDevice failed");
+  }
+  if (dev < 0 || dev >= 64) return fail(ISM_ERR_NO_DEVICE, "device ordinal %d above 63", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(ISM_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ISM_OK;
+}
+
+}  // namespace
+
+extern "C" ism_status ism_attn_decode_noalloc(const void *q, const void *k_new,
+                                              const void *v_new, void *k_cache,
+                                              void *v_cache, int32_t cache_cap,
+                                              const int32_t *cache_seqlens, int32_t batch,
+                                              int32_t max_seqlen, void *o, float *lse,
+                                              int32_t hq, int32_t hkv, int32_t d, float scale,
+                                              int32_t num_splits, void *stream) {
+  ism::clear_error();
+  ism_status st = check_heads(hq, hkv, d, scale);
+  if (st) return st;
+  if (batch < 1 || cache_cap < 1) return fail(ISM_ERR_SHAPE, "need batch >= 1 and cache_cap >= 1");
+  const int32_t ms = max_seqlen == 0 ? cache_cap : max_seqlen;
+  if (ms < 1 || ms > cache_cap)
+    return fail(ISM_ERR_CAPACITY, "max_seqlen %d outside [1, cache_cap=%d]", ms, cache_cap);
+  if (num_splits < 0 || num_splits > 1024)
+    return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
+  const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, ms, hq, hkv, d,
+                                              num_splits);
+  if (need > ISM_NOALLOC_SCRATCH_BYTES)
+    return fail(ISM_ERR_WORKSPACE,
+                "split partials need %zu bytes, above the %zu-byte scratch of the "
+                "allocation-free decode (use ism_attn_decode with a workspace)",
+                need, (size_t)ISM_NOALLOC_SCRATCH_BYTES);
+  if ((st = check_device())) return st;
+  void *ws = nullptr;
+  if ((st = scratch_address(&ws))) return st;
+  return decode_impl(q, k_new, v_new, k_cache, v_cache, cache_cap, cache_seqlens, batch, ms, o,
+                     lse, hq, hkv, d, scale, num_splits, ws, ISM_NOALLOC_SCRATCH_BYTES, stream,
+                     nullptr);
+}

@@ -7,7 +7,7 @@ fallback: if the library is not built or no gfx950 device is present, the
 call fails loudly.
 
 Names follow the C ABI (include/ism_attn.h): fwd, bwd, visibility,
-prefill_cached, prefill_cached_segment, decode,
+prefill_cached, prefill_cached_segment, decode, decode_noalloc,
 prefill_paged, decode_paged, positions_2d, rope2d_, prefill_cached_rope2d,
 plus check_segments_host and workspace_size. Outputs are allocated with
 torch unless the caller passes them (``out=``).
@@ -71,6 +71,8 @@ _SIGS = {
                                    _Z, _P]),
     "ism_attn_decode": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P, _P, _I,
                              _I, _I, _F, _I, _P, _Z, _P]),
+    "ism_attn_decode_noalloc": (_I, [_P, _P, _P, _P, _P, _I, _P, _I, _I, _P,
+                                     _P, _I, _I, _I, _F, _I, _P]),
     "ism_visibility": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P]),
     "ism_positions_2d": (_I, [ctypes.POINTER(ism_segments), _P, _P, _P]),
     "ism_rope2d": (_I, [_P, _I, _I, _I, _I, _P, _P, _F, _I, _P]),
@@ -426,6 +428,22 @@ def decode(q, k_new, v_new, k_cache, v_cache, cache_seqlens, max_seqlen=0,
         _ptr(cache_seqlens), B, ms, _ptr(o), _ptr(lse), hq, hkv, d, scale,
         int(num_splits), _ptr(ws), nws if workspace is None else
         workspace.numel(), _stream()))
+    return o, lse
+
+
+def decode_noalloc(q, k_new, v_new, k_cache, v_cache, cache_seqlens,
+                   max_seqlen=0, scale=None, num_splits=0, return_lse=True,
+                   out=None):
+    """The decode step through ism_attn_decode_noalloc: the library itself
+    allocates nothing (split partials in its fixed per-device scratch);
+    with ``out=(o, lse)`` this wrapper allocates nothing either."""
+    B, hq, hkv, d, cap, scale, o, lse = _decode_args(
+        q, k_new, v_new, k_cache, v_cache, cache_seqlens, scale, return_lse,
+        out)
+    _check(lib().ism_attn_decode_noalloc(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), cap,
+        _ptr(cache_seqlens), B, int(max_seqlen), _ptr(o), _ptr(lse), hq, hkv,
+        d, scale, int(num_splits), _stream()))
     return o, lse
 
 

@@ -121,6 +121,14 @@ def test_cache_argument_errors(L):
     # decode: query heads not a multiple of the KV heads
     assert L.ism_attn_decode(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1, 0, FAKE,
                              None, 3, 2, 64, 0.125, 0, ws, 1 << 20, None) == 2
+    # allocation-free decode: partials beyond the fixed scratch, bad
+    # max_seqlen, bad head dim (all refused before any device access)
+    assert L.ism_attn_decode_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 64, 0,
+                                     FAKE, None, 64, 64, 128, 0.125, 64, None) == 5
+    assert L.ism_attn_decode_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1, 65,
+                                     FAKE, None, 1, 1, 64, 0.125, 0, None) == 6
+    assert L.ism_attn_decode_noalloc(FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, 1, 0,
+                                     FAKE, None, 1, 1, 96, 0.125, 0, None) == 3
     # visibility: outputs required
     sgv = _segs(FAKE, FAKE, FAKE, 1, 1, 10, 10)
     assert L.ism_visibility(ctypes.byref(sgv), None, FAKE, None) == 1
