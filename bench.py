@@ -5,15 +5,21 @@ python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                 [--calibrate-copy]
 
 A step is one training pass of the attention hot path over one batch of
-workload 1 (8 dialogues x 4096 tokens, 32 heads, head_dim 128, bf16): the
-visibility prep, the forward and the backward. ``value`` is the
-useful (unmasked) TFLOP/s of that step: 4*d FLOPs per visible (row, key) pair
-and query head for the forward, 10*d for the backward; ``tokens_per_s`` gives
-the same step as packed tokens per second. The other paths of the hot path
-are measured on their own workloads and reported under ``paths``: the
-grouped-KV forward (workload 2), the cached prefill and the decode stream
-(workload 3, dense and paged, with draft verification, 2-D positions and the
-measured streaming-read ceiling), the backward (workload 4).
+workload 4, the largest training configuration (4 dialogues x 8192 tokens,
+16 turns each, 32 heads, head_dim 128, bf16): the visibility prep, the
+forward (which produces the LSE the backward needs) and the backward.
+``value`` is the useful (unmasked) TFLOP/s of that step: 4*d FLOPs per
+visible (row, key) pair and query head for the forward, 10*d for the
+backward; ``tokens_per_s`` gives the same step as packed tokens per second.
+``roofline`` is the step's backward, the dominant part (its launches timed
+together with HIP events on the launch stream, useful FLOPs only).
+
+The other paths are measured on their own workloads and reported under
+``paths``: the forward and the training step of workload 1 (8 x 4096), the
+grouped-KV forward (workload 2, 2 x 16384, 32/8 heads), the deterministic
+backward of workload 4, the cached prefill and the decode stream (workload
+3, dense and paged, with draft verification, 2-D positions and the measured
+streaming-read ceiling).
 
 Two comparisons from the paper ride along under ``paths``: the training cost
 of the prefix mask's sample expansion against ISM's single pass over the same
@@ -21,15 +27,21 @@ dialogues (Sec. 1), and the per-turn latency experiment of Sec. 3.6 (ISM,
 causal and prefix masks; time to first token and per output token) at the
 level of one attention layer.
 
+``cpu_baseline`` times the fp64 oracle (test infrastructure, as it stands) on
+the host cores, on bounded samples: the step of workload 4 (forward and
+backward of some (dialogue, head) pairs) as the headline figure, and the
+forwards of workloads 1 and 2 and the cache path of workload 3 (one-shot
+reference rows, then 16 stepwise decode steps) beside it.
+
 ``--only gqa|bwd|cache|expansion|latency`` measures that one path alone (for
 per-kernel profiles of one workload) and prints a JSON line with ``paths``
-only.
+only; ``--only step`` runs the headline step alone.
 
 The last line of stdout is one JSON object; everything else goes to stderr.
 
 ``roofline.traffic`` (HBM bytes per launch of the backward) comes from the
 FETCH_SIZE / WRITE_SIZE counter runs recorded in
-``profiles/traffic_step_8x4096_h32_d128.json``, scaled by what the same
+``profiles/traffic_bwd_4x8192_h32_d128.json``, scaled by what the same
 counters read for a plain copy of known size (``--calibrate-copy`` runs that
 copy); it is reported only while the kernel sources hash to the value
 recorded with the counters, else null.
@@ -52,7 +64,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = ("ISM attention useful TFLOP/s (fwd, bwd) and % bf16 MFMA peak; "
           "decode HBM GB/s")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_step_8x4096_h32_d128.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_4x8192_h32_d128.json")
 COPY_BYTES = 1 << 30  # --calibrate-copy: bytes read (and written) per copy
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
@@ -165,11 +177,12 @@ def bench_training(w, timer, steps, warmup, with_bwd):
                   "flop": f_fwd, "tokens_per_s": T / ms_fwd * 1e3}
     if with_bwd:
         do = dev(w.do) if w.do is not None else torch.randn_like(q)
-        ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale),
-                           steps, warmup, WARM_MS)
-        res["bwd"] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
-                      "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
-                      "flop": f_bwd, "tokens_per_s": T / ms_bwd * 1e3}
+        for key, det in (("bwd", False), ("bwd_deterministic", True)):
+            ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale, det),
+                               steps, warmup, WARM_MS)
+            res[key] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
+                        "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
+                        "flop": f_bwd, "tokens_per_s": T / ms_bwd * 1e3}
 
         def step():
             o2, l2 = ops.fwd(q, k, v, segs, w.scale)
@@ -453,37 +466,112 @@ def bench_latency(timer, reps=5, seed=5):
     return {"latency": res}
 
 
-def cpu_baseline(w, budget_s=15.0):
-    """The fp64 oracle forward, as it stands, on a bounded sample of
-    workload 1: the first n (dialogue, head) pairs, n chosen from a one-pair
-    probe so that the run takes about budget_s; one pair per thread."""
-    import oracle
+def _f64(bits):
     from paper_2408_00539_amd.workloads import bf16_bits_to_f32
+    return bf16_bits_to_f32(bits).astype(np.float64)
+
+
+def cpu_baseline(w4, w1=None, w2=None, w3=None):
+    """The fp64 oracle (test infrastructure, as it stands) on bounded samples
+    of the workloads, on the host cores; one (dialogue, head) pair per
+    thread, one BLAS thread each.
+
+    Headline: the training step of workload 4 (oracle forward + backward)
+    on the first `workers` (dialogue, head) pairs, in useful TFLOP/s.
+    Beside it: the forward of workload 1 (all pairs) and of workload 2
+    (`workers` pairs), and workload 3's cache path for one dialogue (the
+    one-shot reference rows of its new query segment and 16 answer tokens,
+    then the same 16 tokens as stepwise decode steps after the cached
+    prefill, as the per-step time and its K/V bytes per second)."""
+    import oracle
     from threadpoolctl import threadpool_limits
     cores = len(os.sched_getaffinity(0))
-    q = bf16_bits_to_f32(w.q).astype(np.float64)
-    k = bf16_bits_to_f32(w.k).astype(np.float64)
-    v = bf16_bits_to_f32(w.v).astype(np.float64)
-    allpairs = [(b, h) for b in range(w.segs.batch) for h in range(w.hq)]
+    workers = max(1, min(cores, 16))
+    out = {"unit": "TFLOP/s", "cores": workers, "kind": "oracle",
+           "cpu": _cpu_model(), "legs": {}}
 
-    def run(pairs):
-        with threadpool_limits(limits=1):
+    def pairs_flop(w, pairs, per_pair):
+        return per_pair * w.d * sum(_pairs_of_dialogue(w.segs, b) for b, _ in pairs)
+
+    with threadpool_limits(limits=1):
+        q, k, v, do = _f64(w4.q), _f64(w4.k), _f64(w4.v), _f64(w4.do)
+        args = (w4.segs.cu_seqlens, w4.segs.cu_segs, w4.segs.seg_is_query, w4.scale)
+        pairs = [(b, h) for b in range(w4.segs.batch) for h in range(w4.hq)][:workers]
+        t0 = time.perf_counter()
+        oracle.fwd(q, k, v, *args, pairs=pairs, workers=workers)
+        oracle.bwd(q, k, v, do, *args, pairs=pairs, workers=workers)
+        dt = time.perf_counter() - t0
+        flop = pairs_flop(w4, pairs, 14)
+        out.update({"value": flop / dt / 1e12, "seconds": round(dt, 2),
+                    "sample": f"fp64 oracle forward + backward of workload 4 (4 x 8192, "
+                              f"32 heads, d 128) on {len(pairs)} of "
+                              f"{w4.segs.batch * w4.hq} (dialogue, head) pairs, "
+                              f"{workers} threads, {dt:.1f} s wall; useful FLOPs "
+                              f"of those pairs (14 d per visible pair)"})
+        del q, k, v, do
+        for name, w, full in (("fwd_8x4096", w1, True), ("fwd_gqa_2x16384", w2, False)):
+            if w is None:
+                continue
+            q, k, v = _f64(w.q), _f64(w.k), _f64(w.v)
+            args = (w.segs.cu_seqlens, w.segs.cu_segs, w.segs.seg_is_query, w.scale)
+            pairs = [(b, h) for b in range(w.segs.batch) for h in range(w.hq)]
+            if not full:
+                pairs = pairs[:workers]
             t0 = time.perf_counter()
-            oracle.fwd(q, k, v, w.segs.cu_seqlens, w.segs.cu_segs,
-                       w.segs.seg_is_query, w.scale, pairs=pairs,
-                       workers=min(cores, len(pairs)))
-            return time.perf_counter() - t0
+            oracle.fwd(q, k, v, *args, pairs=pairs, workers=workers)
+            dt = time.perf_counter() - t0
+            out["legs"][name] = {"value": pairs_flop(w, pairs, 4) / dt / 1e12,
+                                 "unit": "TFLOP/s", "seconds": round(dt, 2),
+                                 "pairs": len(pairs),
+                                 "of_pairs": w.segs.batch * w.hq}
+            del q, k, v
+        if w3 is not None:
+            out["legs"]["cache_32x8192"] = _cpu_cache_leg(oracle, w3, workers)
+    return out
 
-    t1 = run(allpairs[:1])
-    n = int(min(len(allpairs), max(1, cores * int(budget_s / max(t1, 1e-3)))))
-    dt = run(allpairs[:n])
-    flop = 4 * w.d * sum(_pairs_of_dialogue(w.segs, b) for b, _ in allpairs[:n])
-    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"fp64 numpy oracle forward on {n} of {len(allpairs)} "
-                      f"(dialogue, head) pairs of workload 1, one pair per "
-                      f"thread, {dt:.1f} s wall",
-            "seconds": round(dt, 2), "cpu": _cpu_model()}
+
+def _cpu_cache_leg(oracle, w, workers, steps=16):
+    """One dialogue of workload 3: the one-shot oracle forward of its new
+    query segment and `steps` answer tokens over [history; Q_n; A_n] (the
+    reference rows of the parity tests), and the stepwise path: cached
+    prefill, then `steps` decode steps, each appending its key / value."""
+    from concurrent.futures import ThreadPoolExecutor
+    from paper_2408_00539_amd import workloads as W
+    b, C, L = 0, w.hist_len, int(w.new_lens[0])
+    r0, r1 = int(w.cu_new[0]), int(w.cu_new[1])
+    kh = _f64(w.k_cache[0, :, :C]).transpose(1, 0, 2)
+    vh = _f64(w.v_cache[0, :, :C]).transpose(1, 0, 2)
+    qn, kn, vn = _f64(w.q_new[r0:r1]), _f64(w.k_new[r0:r1]), _f64(w.v_new[r0:r1])
+    qd, kd, vd = (_f64(x[:steps, b]) for x in (w.q_dec, w.k_dec, w.v_dec))
+    dia = W.segments_from_lengths([
+        [(int(n), bool(f)) for n, f in zip(np.diff(w.hist.cu_segs[:33]),
+                                            w.hist.seg_is_query[:32])]
+        + [(L, True), (steps, False)]])
+    n = C + L + steps
+    qq = np.zeros((n, w.hq, w.d))
+    qq[C:C + L], qq[C + L:] = qn, qd
+    kk = np.concatenate([kh, kn, kd])
+    vv = np.concatenate([vh, vn, vd])
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(workers) as ex:
+        list(ex.map(lambda h: oracle.fwd_rows(qq, kk, vv, dia.cu_seqlens, dia.cu_segs,
+                                              dia.seg_is_query, w.scale, 0, h,
+                                              rows=(C, n)), range(w.hq)))
+    t_one = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    _, _, kc, vc = oracle.prefill_cached(kh, vh, qn, kn, vn, w.scale)
+    t_pf = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    for t in range(steps):
+        _, _, kc, vc = oracle.decode_step(kc, vc, qd[t], kd[t], vd[t], w.scale)
+    t_dec = (time.perf_counter() - t0) / steps
+    kv_bytes = 2 * w.hkv * w.d * 2 * (C + L + steps / 2 + 0.5)  # bf16 K+V per step
+    return {"dialogues": 1, "of_dialogues": len(w.new_lens), "decode_steps": steps,
+            "one_shot_rows_s": round(t_one, 3), "prefill_s": round(t_pf, 3),
+            "decode_ms_per_step": round(1e3 * t_dec, 2),
+            "decode_equiv_gbs": kv_bytes / t_dec / 1e9,
+            "note": "one-shot rows use a thread per head; the stepwise path runs "
+                    "on one thread"}
 
 
 def _pairs_of_dialogue(segs, b):
@@ -678,7 +766,6 @@ def main():
         calibrate_copy()
         return
     timer = Timer()
-    with_bwd = True
     if args.only in ("gqa", "bwd", "cache", "expansion", "latency"):
         paths = {}
         if args.only == "gqa":
@@ -689,6 +776,8 @@ def main():
             w4 = W.make_workload(4)
             t4 = bench_training(w4, timer, 5, 1, True)
             paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
+            paths["bwd_deterministic"] = dict(t4["bwd_deterministic"],
+                                              workload="4x8192 h32 d128")
         elif args.only == "cache":
             paths.update(bench_cache(W.make_workload(3), timer, 8, 2))
         elif args.only == "expansion":
@@ -701,39 +790,36 @@ def main():
         print(json.dumps({"paths": paths}), flush=True)
         return
 
-    log("generating workload 1 ...")
-    w1 = W.make_workload(1)
-    if with_bwd:
-        w1.do = W.packed_tensor(w1.seed, W.DO, w1.segs.cu_seqlens, w1.hq, w1.d)
+    # the headline: the training step of workload 4
+    log("generating workload 4 ...")
+    w4 = W.make_workload(4)
     torch.cuda.synchronize()
-    tr = bench_training(w1, timer, args.steps, args.warmup, with_bwd)
+    tr = bench_training(w4, timer, args.steps, args.warmup, True)
     step_ms, step_flop = tr["step"]["ms"], tr["step"]["flop"]
     log(f"step: {step_ms:.3f} ms, {step_flop / step_ms / 1e9:.1f} TFLOP/s")
-
-    paths = {"fwd": dict(tr["fwd"], workload="8x4096 h32 d128")}
-    dom_name, dom = "fwd_kernel", tr["fwd"]
-    if with_bwd:
-        paths["bwd_8x4096"] = dict(tr["bwd"], workload="8x4096 h32 d128")
-        dom_name, dom = "ism_attn_bwd (delta_kernel + dkv_kernel + dq_kernel)", tr["bwd"]
+    paths = {"fwd_4x8192": dict(tr["fwd"], workload="4x8192 h32 d128"),
+             "bwd": dict(tr["bwd"], workload="4x8192 h32 d128"),
+             "bwd_deterministic": dict(tr["bwd_deterministic"], workload="4x8192 h32 d128")}
+    dom = tr["bwd"]
+    w1 = w2 = w3 = None
     if args.only == "all":
+        log("generating workload 1 ...")
+        w1 = W.make_workload(1)
+        w1.do = W.packed_tensor(w1.seed, W.DO, w1.segs.cu_seqlens, w1.hq, w1.d)
+        t1 = bench_training(w1, timer, 10, 2, True)
+        paths["fwd"] = dict(t1["fwd"], workload="8x4096 h32 d128")
+        paths["step_8x4096"] = dict(t1["step"], workload="8x4096 h32 d128 (prep+fwd+bwd)")
+        paths["bwd_8x4096"] = dict(t1["bwd"], workload="8x4096 h32 d128")
         log("generating workload 2 ...")
         w2 = W.make_workload(2)
         t2 = bench_training(w2, timer, 10, 2, False)
         paths["fwd_gqa"] = dict(t2["fwd"], workload="2x16384 h32/kv8 d128")
-        del w2
-        if with_bwd:
-            log("generating workload 4 ...")
-            w4 = W.make_workload(4)
-            t4 = bench_training(w4, timer, 5, 1, True)
-            paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
-            del w4
         log("generating workload 3 ...")
         w3 = W.make_workload(3)
         paths.update(bench_cache(w3, timer, 8, 2))
-        del w3
         torch.cuda.empty_cache()
-        log("prefix-mask expansion of the step's dialogues ...")
-        paths.update(bench_expansion(w1, timer, 3, 1, step_ms))
+        log("prefix-mask expansion of workload 1's dialogues ...")
+        paths.update(bench_expansion(w1, timer, 3, 1, t1["step"]["ms"]))
         torch.cuda.empty_cache()
         log("latency turns ...")
         paths.update(bench_latency(timer))
@@ -742,7 +828,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
-        cpu = cpu_baseline(w1)
+        cpu = cpu_baseline(w4, w1, w2, w3)
 
     value = step_flop / step_ms / 1e9
     line = {
@@ -759,23 +845,22 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "ISM training step (prep+fwd" +
-                   ("+bwd" if with_bwd else "") + "), 8 dialogues x 4096 "
-                   "tokens, 8 turns, 32 heads, head_dim 128",
-                   "global_batch": 8, "seq_len": 4096, "heads": 32,
+        "config": {"workload": "ISM training step (prep + forward with LSE + backward), "
+                   "4 dialogues x 8192 tokens, 16 turns, 32 heads, head_dim 128",
+                   "global_batch": 4, "seq_len": 8192, "heads": 32,
                    "head_dim": 128, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "mfma", "kernel": dom_name,
+        "roofline": {"bound": "mfma",
+                     "kernel": "ism_attn_bwd on the step's inputs (all its launches)",
                      "achieved": round(dom["tflops"], 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(dom["tflops"] / PEAK_BF16_TFLOPS, 4),
-                     "traffic": recorded_traffic() if with_bwd else None},
+                     "traffic": recorded_traffic()},
         "cpu_baseline": cpu,
         "device": device_info(),
         "paths": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                       for kk, vv in v.items()} for k, v in paths.items()},
     }
     print(json.dumps(line), flush=True)
-
 
 if __name__ == "__main__":
     main()
