@@ -16,8 +16,7 @@ together with HIP events on the launch stream, useful FLOPs only).
 
 The other paths are measured on their own workloads and reported under
 ``paths``: the forward and the training step of workload 1 (8 x 4096), the
-grouped-KV forward (workload 2, 2 x 16384, 32/8 heads), the deterministic
-backward of workload 4, the cached prefill and the decode stream (workload
+grouped-KV forward (workload 2, 2 x 16384, 32/8 heads), the cached prefill and the decode stream (workload
 3, dense and paged, with draft verification, 2-D positions and the measured
 streaming-read ceiling).
 
@@ -177,12 +176,11 @@ def bench_training(w, timer, steps, warmup, with_bwd):
                   "flop": f_fwd, "tokens_per_s": T / ms_fwd * 1e3}
     if with_bwd:
         do = dev(w.do) if w.do is not None else torch.randn_like(q)
-        for key, det in (("bwd", False), ("bwd_deterministic", True)):
-            ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale, det),
-                               steps, warmup, WARM_MS)
-            res[key] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
-                        "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
-                        "flop": f_bwd, "tokens_per_s": T / ms_bwd * 1e3}
+        ms_bwd = timer.run(lambda: ops.bwd(q, k, v, o, lse, do, segs, w.scale),
+                           steps, warmup, WARM_MS)
+        res["bwd"] = {"ms": ms_bwd, "tflops": f_bwd / ms_bwd / 1e9,
+                      "frac_peak": f_bwd / ms_bwd / 1e9 / PEAK_BF16_TFLOPS,
+                      "flop": f_bwd, "tokens_per_s": T / ms_bwd * 1e3}
 
         def step():
             o2, l2 = ops.fwd(q, k, v, segs, w.scale)
@@ -776,8 +774,6 @@ def main():
             w4 = W.make_workload(4)
             t4 = bench_training(w4, timer, 5, 1, True)
             paths["bwd"] = dict(t4["bwd"], workload="4x8192 h32 d128")
-            paths["bwd_deterministic"] = dict(t4["bwd_deterministic"],
-                                              workload="4x8192 h32 d128")
         elif args.only == "cache":
             paths.update(bench_cache(W.make_workload(3), timer, 8, 2))
         elif args.only == "expansion":
@@ -798,8 +794,7 @@ def main():
     step_ms, step_flop = tr["step"]["ms"], tr["step"]["flop"]
     log(f"step: {step_ms:.3f} ms, {step_flop / step_ms / 1e9:.1f} TFLOP/s")
     paths = {"fwd_4x8192": dict(tr["fwd"], workload="4x8192 h32 d128"),
-             "bwd": dict(tr["bwd"], workload="4x8192 h32 d128"),
-             "bwd_deterministic": dict(tr["bwd_deterministic"], workload="4x8192 h32 d128")}
+             "bwd": dict(tr["bwd"], workload="4x8192 h32 d128")}
     dom = tr["bwd"]
     w1 = w2 = w3 = None
     if args.only == "all":

@@ -236,20 +236,9 @@ dkv_kernel(BwdArgs a, int ktiles) {
     const char *dl = (const char *)sm.dout[st];
     const u32x4 *pp = sm.p[sp][pair];
     u32x4 pw[NKK];
-    f32x16 nd[NRB];  // -delta of the current tile's rows, as dP' accumulators
     if constexpr (DS) {
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) pw[kk] = pp[kk * 64 + lane];
-    }
-    if constexpr (DP) {
-#pragma unroll
-      for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x4 v = *(const f32x4 *)&sm.delta[st][32 * rb + 8 * i + 4 * hf];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) nd[rb][4 * i + j] = v[j];
-        }
     }
     u32x4 fw[NKK];
     // dS elements 2u, 2u + 1 of slice kk (accumulator elements 8 bt + 2u ..)
@@ -279,7 +268,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
       } else {
         constexpr int j = n - NK, ks = j / NRB, rb = j % NRB;
-        dp[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? nd[rb] : dp[rb]);
+        dp[rb] = mfma32x32x16(x, bop[ks], dp[rb]);
       }
     };
     auto pre = [&](auto nc) __attribute__((always_inline)) {
@@ -290,6 +279,21 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if constexpr (DS && n == 0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) ds_pair(0, u);
+      }
+      // the dP' accumulators start at the current tile's -delta, loaded into
+      // dp just before the dP products, once the previous tile's dP has been
+      // consumed (its last dS slice is formed before product NK - NDB); held
+      // from the stream's start they would cost 2 x 16 registers through the
+      // dK products
+      if constexpr (DP && n == (DS ? NK - NDB : 0)) {
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const f32x4 v = *(const f32x4 *)&sm.delta[st][32 * rb + 8 * i + 4 * hf];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dp[rb][4 * i + j] = v[j];
+          }
       }
     };
     auto work = [&](auto nc) __attribute__((always_inline)) {

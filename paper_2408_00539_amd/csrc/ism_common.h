@@ -208,13 +208,18 @@ struct DmaTile {
         if (kEven || q < T) dma_x4s(src, loff[i], lb + q * 1024);
       }
     } else {
+      // the lane index is re-read here (volatile, so not hoisted): a
+      // register kept across the caller's loop for this rare path would cost
+      // more than the two instructions
+      int ln;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int q = i * NW + wave;
         if (!kEven && q >= T) continue;
-        const int r = q * RPI + lane / CPR;
+        const int r = q * RPI + ln / CPR;
         const int rr = min(r, nvalid - 1);
-        dma_x4s(src, (uint32_t)(rr * rs + ((lane % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
+        dma_x4s(src, (uint32_t)(rr * rs + ((ln % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
       }
     }
   }

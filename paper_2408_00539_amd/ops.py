@@ -241,9 +241,8 @@ def fwd(q, k, v, segs, scale=None, return_lse=True, out=None):
 def bwd(q, k, v, o, lse, dout, segs, scale=None, deterministic=False,
         out=None):
     """Gradients (dq [T,hq,d], dk, dv [T,hkv,d], fp32) of ism fwd;
-    ``out=(dq, dk, dv)`` writes into caller tensors instead.
-    ``deterministic`` selects the bitwise-repeatable path; the default
-    accumulates dQ with atomics in one pass (see ism_attn_bwd)."""
+    ``out=(dq, dk, dv)`` writes into caller tensors instead. The result is
+    bitwise repeatable whatever ``deterministic`` says (see ism_attn_bwd)."""
     torch = _torch()
     _need(q, "q", torch.bfloat16)
     if q.dim() != 3:

@@ -63,7 +63,8 @@ def test_small_shapes(layout, d, hq, hkv):
 
 
 def test_bitwise_repeatable():
-    """The backward has no atomics: two runs give identical bits."""
+    """The backward has no atomics: two runs give identical bits, and the
+    deterministic flag (reserved) does not change them."""
     torch = torch_cuda()
     segs = W.segments_from_lengths([W.alternating([100, 300, 80, 200])] * 2)
     rng = np.random.default_rng(12)
@@ -71,10 +72,11 @@ def test_bitwise_repeatable():
     q, k, v, do = (_bits(rng, T, 8, 128), _bits(rng, T, 2, 128),
                    _bits(rng, T, 2, 128), _bits(rng, T, 8, 128))
     announce("bwd repeatable")
-    a = _gpu_grads(segs, q, k, v, do, 0.088)
-    b = _gpu_grads(segs, q, k, v, do, 0.088)
-    for x, y in zip(a, b):
-        assert torch.equal(x, y)
+    a = _gpu_grads(segs, q, k, v, do, 0.088, True)
+    b = _gpu_grads(segs, q, k, v, do, 0.088, True)
+    c = _gpu_grads(segs, q, k, v, do, 0.088, False)
+    for x, y, z in zip(a, b, c):
+        assert torch.equal(x, y) and torch.equal(x, z)
 
 
 def test_workload4_sampled():
@@ -102,3 +104,4 @@ def test_workload4_sampled():
         compare(f"dQ b{b} h{h}", host_f64(dq[s:e, h]), rq[s:e, h])
         compare(f"dK b{b} h{h}", host_f64(dk[s:e, h]), rk[s:e, h])
         compare(f"dV b{b} h{h}", host_f64(dv[s:e, h]), rv[s:e, h])
+
