@@ -661,7 +661,7 @@ def write_traffic_record(fetch_copy, fetch_step, write_copy, write_step,
     sf = COPY_BYTES / 1024 / copy_f
     sw = COPY_BYTES / 1024 / copy_w
     rec = {"kernel_source_sha256": kernel_source_hash(),
-           "workload": "training step, 8 dialogues x 4096 tokens, 32 heads, "
+           "workload": "training step, 4 dialogues x 8192 tokens, 32 heads, "
                        "head_dim 128 (cache path: 32 x 8192, 32 heads)",
            "copy_calibration": {"copy_bytes": COPY_BYTES,
                                 "FETCH_SIZE_KiB": round(copy_f, 1),

@@ -183,10 +183,12 @@ __device__ __forceinline__ void tile_pv(const char *vl, const SwzOffsets<D> &so,
 }
 
 // One pipelined step in a fixed instruction order: the D/8 products of
-// S(t+1) = K(t+1) Q^T, then the D/8 products of O^T += V(t)^T P(t)^T (64-key
-// chunks outermost, so consecutive products use different accumulators).
-// Each product is followed by the LDS read of the operand LA products ahead
-// (K rows, then transposed V) and by its share of the vector work: during
+// S(t+1) = K(t+1) Q^T (its two 32-key blocks alternating), then the D/8
+// products of O^T += V(t)^T P(t)^T (64-key chunks outermost), so that
+// consecutive products always use different accumulators. Each product is
+// followed by the LDS read of the operand LA = 2 products ahead (K rows, then
+// transposed V; a third operand in flight measured ~1 % slower, one only
+// ~7 % slower) and by its share of the vector work: during
 // the S products the exponentials, row sums and bf16 packing of tile t,
 // during the P V products the row max of S(t+1). The order is pinned with
 // scheduling barriers so that the matrix core and the vector ALU of a wave
@@ -200,12 +202,12 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
                                             f32x16 (&oacc)[D / 32], float sl2, float moff,
                                             float &mt, Hook &&hook) {
   constexpr int NKS = D / 16, NDB = D / 32;
-  constexpr int NS = 2 * NKS, NP = 4 * NDB, N = NS + NP, LA = 3;
+  constexpr int NS = 2 * NKS, NP = 4 * NDB, N = NS + NP, LA = 2;
   constexpr int PPS = 16 / NS;  // probability pairs per S product
   constexpr int MPP = 32 / NP;  // max elements per P V product
   auto read = [&](int n) -> bf16x8 {
     if (n < NS) {
-      const int kb = n / NKS, ks = n % NKS;
+      const int kb = n & 1, ks = n >> 1;
       return *(const bf16x8 *)(kl + kb * 32 * D * 2 + so.rowk[ks]);
     }
     const int j = n - NS, kc = j / NDB, db = j % NDB;
@@ -222,7 +224,7 @@ __device__ __forceinline__ float step_block(const char *kl, const char *vl,
   for (int n = 0; n < N; ++n) {
     if (n < NS) {
       if (!LAST) {
-        const int kb = n / NKS, ks = n % NKS;
+        const int kb = n & 1, ks = n >> 1;
         nxt[kb] = mfma32x32x16(op[n], qf[ks], ks == 0 ? f32x16{} : nxt[kb]);
       }
     } else {

@@ -105,3 +105,25 @@ def test_workload4_sampled():
         compare(f"dK b{b} h{h}", host_f64(dk[s:e, h]), rk[s:e, h])
         compare(f"dV b{b} h{h}", host_f64(dv[s:e, h]), rv[s:e, h])
 
+
+
+def test_mismatched_shapes_raise_before_launch():
+    """ops.bwd checks every tensor's shape and the token count against the
+    segments before the library is called."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    segs_h = W.segments_from_lengths([W.alternating([20, 30])])
+    segs = ops.Segments.from_host(segs_h.cu_seqlens, segs_h.cu_segs, segs_h.seg_is_query)
+    T, hq, hkv, d = segs_h.total, 4, 2, 64
+    z = lambda *s: torch.zeros(s, dtype=torch.bfloat16, device="cuda")
+    q, k, v, o, do = z(T, hq, d), z(T, hkv, d), z(T, hkv, d), z(T, hq, d), z(T, hq, d)
+    lse = torch.zeros((hq, T), dtype=torch.float32, device="cuda")
+    bad = {"k": (q, z(T - 1, hkv, d), v, o, lse, do), "v": (q, k, z(T, hkv, d + 64), o, lse, do),
+           "o": (q, k, v, z(T, hq - 1, d), lse, do), "dout": (q, k, v, o, lse, z(T + 1, hq, d))}
+    for name, args in bad.items():
+        with pytest.raises(ValueError, match=name):
+            ops.bwd(*args, segs)
+    other = ops.Segments.from_host(np.array([0, T - 1]), np.array([0, 20, T - 1]),
+                                   np.array([1, 0]))
+    with pytest.raises(ValueError, match="total_tokens"):
+        ops.bwd(q, k, v, o, lse, do, other)
