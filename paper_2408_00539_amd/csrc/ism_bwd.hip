@@ -7,8 +7,10 @@
 //     (every later row of the dialogue sees i as well, since lim is
 //     non-decreasing inside a dialogue and lim(j) >= j).
 //  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji),
-//     stored negated so that the dK/dV kernel starts its dP accumulators at
-//     -delta and forms dS = P o dP' without a subtraction.
+//     stored negated so that the dP accumulators start at -delta and
+//     dS = P o dP' needs no subtraction; for the dK/dV kernel -delta and
+//     -lse / scale are also stored as sums of three bf16 values, which one
+//     product per row block adds to every key of the block's rows.
 //  3. dK/dV kernel, key-tile outer: a workgroup owns 128 keys of one KV head
 //     (32 per wave pair, lane <-> key), walks the query heads of the group
 //     and the 64-row tiles from seer[first key] to the dialogue end, and
@@ -53,13 +55,28 @@ bwd_prep_kernel(const int32_t *__restrict__ cu_segs,
   seer[j] = q ? cu_segs[lo] : j;
 }
 
+// c as the exact sum of three bf16 values: c truncated to bf16, the
+// remainder truncated, and the rest (at most 8 significant bits, so exact).
+// Word 0 holds the first two (low half first), word 1 the third and zero.
+__device__ __forceinline__ void split3_bf16(float c, uint32_t &w0, uint32_t &w1) {
+  const uint32_t b0 = __float_as_uint(c) & 0xffff0000u;
+  const float r1 = c - __uint_as_float(b0);
+  const uint32_t b1 = __float_as_uint(r1) & 0xffff0000u;
+  const float r2 = r1 - __uint_as_float(b1);
+  w0 = (b0 >> 16) | b1;
+  w1 = __float_as_uint(r2) >> 16;
+}
+
 // -delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads; also the
-// LSE in log2 units (lse * log2 e) that the dK/dV kernel stages per tile.
+// LSE in log2 units (lse * log2 e) for the dQ kernel, and -lse / scale and
+// -delta split into bf16 summands for the dK/dV kernel, which adds them to
+// its S and dP accumulators with one product each.
 template <int D>
 __global__ void __launch_bounds__(256)
 delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
              const float *__restrict__ lse, float *__restrict__ delta,
-             float *__restrict__ lse2, int32_t total, int32_t hq) {
+             float *__restrict__ lse2, uint32_t *__restrict__ lsex,
+             uint32_t *__restrict__ deltax, float inv_scale, int32_t total, int32_t hq) {
   constexpr int LPR = D / 8;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t pairs = (int64_t)total * hq;
@@ -78,8 +95,16 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
   for (int s = 1; s < LPR; s <<= 1) acc += __shfl_xor(acc, s);
   if (c == 0 && gid / LPR < pairs) {
     const int64_t row = rh / hq, h = rh % hq;
+    const float l = lse[h * total + row];
     delta[h * total + row] = -acc;
-    lse2[h * total + row] = lse[h * total + row] * kLog2e;
+    lse2[h * total + row] = l * kLog2e;
+    uint32_t w0, w1;
+    split3_bf16(-l * inv_scale, w0, w1);
+    lsex[2 * h * total + row] = w0;
+    lsex[(2 * h + 1) * total + row] = w1;
+    split3_bf16(-acc, w0, w1);
+    deltax[2 * h * total + row] = w0;
+    deltax[(2 * h + 1) * total + row] = w1;
   }
 }
 
@@ -90,16 +115,16 @@ delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
 constexpr int kDkvStages = 3;
 
 // Q and dO tiles of 64 rows (unpadded swizzled rows, see swz<D>()) plus the
-// per-row LSE (log2 units) and delta, all filled by direct global->LDS
-// transfers; and P of the last two tiles for each wave pair in the bf16 B
+// per-row -lse / scale and -delta as two planes of bf16 summands, all filled
+// by direct global->LDS transfers; and P of the last two tiles for each wave pair in the bf16 B
 // operand form of the dV product (lane-private, 4 x 16 bytes per lane, laid
 // out so that consecutive lanes touch consecutive bytes).
 template <int D>
 struct DkvSmem {
   bf16_t q[kDkvStages][kBR * D];
   bf16_t dout[kDkvStages][kBR * D];
-  __attribute__((aligned(16))) float lse2[kDkvStages][kBR];
-  __attribute__((aligned(16))) float delta[kDkvStages][kBR];
+  __attribute__((aligned(16))) uint32_t lsex[kDkvStages][2][kBR];
+  __attribute__((aligned(16))) uint32_t deltax[kDkvStages][2][kBR];
   __attribute__((aligned(16))) u32x4 p[kDkvStages][4][4 * 64];
 };
 
@@ -195,8 +220,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
     const int64_t base = ((int64_t)r0 * a.hq + nx_h) * D;
     dma.issue((const bf16_t *)a.q + base, rs, e - r0, sm.q[st]);
     dma.issue((const bf16_t *)a.dout + base, rs, e - r0, sm.dout[st]);
-    if (wave == 6) dma_row_scalars(a.lse2 + (int64_t)nx_h * a.total, r0, e - 1, sm.lse2[st], lane);
-    if (wave == 7) dma_row_scalars(a.delta + (int64_t)nx_h * a.total, r0, e - 1, sm.delta[st], lane);
+    if (wave >= 4) {  // one plane of the split -lse / scale or -delta per dS wave
+      const int pl = wave & 1;
+      const uint32_t *src = (wave < 6 ? a.lsex : a.deltax) + (int64_t)(2 * nx_h + pl) * a.total;
+      dma_row_scalars(src, r0, e - 1, wave < 6 ? sm.lsex[st][pl] : sm.deltax[st][pl], lane);
+    }
     ++nx;
     if (++nx_rt == nrt) { nx_rt = 0; ++nx_h; }
   };
@@ -214,6 +242,13 @@ dkv_kernel(BwdArgs a, int ktiles) {
     issue_next(0);
     wait_loads();  // also drains the first transfer
   }
+  // B operand of the products that add a row's -lse / scale (P wave) or
+  // -delta (dS wave) to every key of its row: 1 in the k slots 0-2 (lanes
+  // 0-31 hold k = 0-7), 0 elsewhere; the matching A operand holds the row's
+  // three bf16 summands in those slots (split3_bf16).
+  const bf16x8 ones3 = __builtin_bit_cast(
+      bf16x8, hf ? u32x4{0u, 0u, 0u, 0u} : u32x4{0x3f803f80u, 0x3f80u, 0u, 0u});
+  const int l32 = lane & 31;
   f32x16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = f32x16{};
@@ -222,16 +257,26 @@ dkv_kernel(BwdArgs a, int ktiles) {
   for (int rb = 0; rb < NRB; ++rb) dp[rb] = f32x16{};
   bool vis_prev = false;  // dS wave: the previous tile had visible keys
 
+  // A operand of the product that adds row (32 rb + lane % 32)'s summands
+  // (plane 0: two bf16, plane 1: the third and zero) to a 32-row block
+  auto summands = [&](const uint32_t (*pl)[kBR], int rb) __attribute__((always_inline)) {
+    const int r = 32 * rb + l32;
+    return __builtin_bit_cast(bf16x8, u32x4{pl[0][r], pl[1][r], 0u, 0u});
+  };
+
   // dS wave, one product stream per step: for the previous tile (stage sp,
   // also its P buffer) dS = P o dP' in 16-row slices, each slice's
   // dK^T[d][key] += Q^T[d][row] dS[row][key] products running beside the
   // elementwise work of the next slice; then (DP) dP'[row][key] = dO V^T -
-  // delta of the current tile (stage st), the accumulators starting at the
-  // staged -delta. The empty asm statements keep each slot's vector work in
-  // its slot (IR passes would otherwise sink it to its use).
+  // delta of the current tile (stage st): one product per 32-row block
+  // starts each accumulator at the row's -delta (it runs after the last dS
+  // slice has consumed the previous dP), then the dO V^T products. The
+  // empty asm statements keep each slot's vector work in its slot (IR
+  // passes would otherwise sink it to its use).
   auto ds_dp = [&](int sp, int st, auto has_ds, auto has_dp) __attribute__((always_inline)) {
     constexpr bool DS = decltype(has_ds)::value, DP = decltype(has_dp)::value;
-    constexpr int NK = DS ? NKK * NDB : 0, N = NK + (DP ? NKS * NRB : 0);
+    constexpr int NK = DS ? NKK * NDB : 0, NX = DP ? NRB : 0;
+    constexpr int N = NK + NX + (DP ? NKS * NRB : 0);
     const char *ql = (const char *)sm.q[sp];
     const char *dl = (const char *)sm.dout[st];
     const u32x4 *pp = sm.p[sp][pair];
@@ -256,8 +301,10 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if constexpr (n < NK) {  // n = kk * NDB + db
         constexpr int kk = n / NDB, db = n % NDB;
         return tr_operand_at(ql, 16 * kk * RB + so.tr(db, 0), 16 * kk * RB + so.tr(db, 1));
-      } else {  // n - NK = ks * NRB + rb
-        constexpr int j = n - NK;
+      } else if constexpr (n < NK + NX) {
+        return summands(sm.deltax[st], n - NK);
+      } else {  // n - NK - NX = ks * NRB + rb
+        constexpr int j = n - NK - NX;
         return *(const bf16x8 *)(dl + (j % NRB) * 32 * RB + so.row(j / NRB));
       }
     };
@@ -266,8 +313,10 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if constexpr (n < NK) {
         constexpr int kk = n / NDB, db = n % NDB;
         acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
+      } else if constexpr (n < NK + NX) {
+        dp[n - NK] = mfma32x32x16(x, ones3, f32x16{});
       } else {
-        constexpr int j = n - NK, ks = j / NRB, rb = j % NRB;
+        constexpr int j = n - NK - NX, ks = j / NRB, rb = j % NRB;
         dp[rb] = mfma32x32x16(x, bop[ks], dp[rb]);
       }
     };
@@ -279,21 +328,6 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if constexpr (DS && n == 0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) ds_pair(0, u);
-      }
-      // the dP' accumulators start at the current tile's -delta, loaded into
-      // dp just before the dP products, once the previous tile's dP has been
-      // consumed (its last dS slice is formed before product NK - NDB); held
-      // from the stream's start they would cost 2 x 16 registers through the
-      // dK products
-      if constexpr (DP && n == (DS ? NK - NDB : 0)) {
-#pragma unroll
-        for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const f32x4 v = *(const f32x4 *)&sm.delta[st][32 * rb + 8 * i + 4 * hf];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) dp[rb][4 * i + j] = v[j];
-          }
       }
     };
     auto work = [&](auto nc) __attribute__((always_inline)) {
@@ -309,9 +343,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
   };
 
   // P wave on the current tile (stage st, rows r0.., nvalid valid), one
-  // product stream: S of row block 0, S of row block 1 beside the
-  // exponentials of block 0, dV^T += dO^T P for block 0 beside the
-  // exponentials of block 1, then dV for block 1. P goes to LDS (and into
+  // product stream: one product per row block that starts its accumulator
+  // at the row's -lse / scale (so that P = exp2(acc * scale * log2 e)), S
+  // of row block 0, S of row block 1 beside the exponentials of block 0,
+  // dV^T += dO^T P for block 0 beside the exponentials of block 1, then dV
+  // for block 1. P goes to LDS (and into
   // operand form) in 16-row slices; rows are masked unless every row sees
   // every key.
   auto p_dv = [&](int st, int r0, int nvalid, bool full) __attribute__((always_inline)) {
@@ -320,12 +356,14 @@ dkv_kernel(BwdArgs a, int ktiles) {
     u32x4 *pp = sm.p[st][pair];
     f32x16 sacc[NRB];
     u32x4 fw[NKK];
-    f32x4 l2[NRB][4];
+    constexpr int NX = NRB;        // summand products, then
     constexpr int NS = NKS * NRB;  // S products, row-block major
     constexpr int EPS = 16 / NKS;  // exponentials per slot
     auto rd = [&](auto nc) __attribute__((always_inline)) -> bf16x8 {
-      constexpr int n = decltype(nc)::value;
-      if constexpr (n < NS) {
+      constexpr int n = decltype(nc)::value - NX;
+      if constexpr (n < 0) {
+        return summands(sm.lsex[st], n + NX);
+      } else if constexpr (n < NS) {
         return *(const bf16x8 *)(ql + (n / NKS) * 32 * RB + so.row(n % NKS));
       } else {  // n - NS = kk * NDB + db
         constexpr int kk = (n - NS) / NDB, db = (n - NS) % NDB;
@@ -333,10 +371,12 @@ dkv_kernel(BwdArgs a, int ktiles) {
       }
     };
     auto mm = [&](auto nc, bf16x8 x) __attribute__((always_inline)) {
-      constexpr int n = decltype(nc)::value;
-      if constexpr (n < NS) {
+      constexpr int n = decltype(nc)::value - NX;
+      if constexpr (n < 0) {
+        sacc[n + NX] = mfma32x32x16(x, ones3, f32x16{});
+      } else if constexpr (n < NS) {
         constexpr int rb = n / NKS, ks = n % NKS;
-        sacc[rb] = mfma32x32x16(x, bop[ks], ks == 0 ? f32x16{} : sacc[rb]);
+        sacc[rb] = mfma32x32x16(x, bop[ks], sacc[rb]);
       } else {
         constexpr int kk = (n - NS) / NDB, db = (n - NS) % NDB;
         acc[db] = mfma32x32x16(x, __builtin_bit_cast(bf16x8, fw[kk]), acc[db]);
@@ -355,29 +395,22 @@ dkv_kernel(BwdArgs a, int ktiles) {
       if constexpr (n == 2) {
         if (nx < iters) issue_next((st + 1) % kDkvStages);
       }
-      if constexpr (n == 0) {
-#pragma unroll
-        for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            l2[rb][i] = *(const f32x4 *)&sm.lse2[st][32 * rb + 8 * i + 4 * hf];
-      }
-      if constexpr (n == NKS || n == 2 * NKS) {
-        if (!full) mask_rb(n / NKS - 1);
+      if constexpr (n == NX + NKS || n == NX + 2 * NKS) {
+        if (!full) mask_rb((n - NX) / NKS - 1);
       }
     };
     // exponentials of block rb in the NKS slots after its S is complete;
     // each finished 16-row slice goes to LDS and operand form
     auto work = [&](auto nc) __attribute__((always_inline)) {
-      constexpr int n = decltype(nc)::value;
+      constexpr int n = decltype(nc)::value - NX;
       if constexpr (n >= NKS && n < 3 * NKS) {
         constexpr int rb = n / NKS - 1, w = n % NKS;
 #pragma unroll
         for (int c = 0; c < EPS; c += 2) {
           const int e0 = w * EPS + c;  // accumulator elements e0, e0 + 1
           f32x2 x;
-          x[0] = fast_exp2(fmaf(sacc[rb][e0], sl2, -l2[rb][e0 >> 2][e0 & 3]));
-          x[1] = fast_exp2(fmaf(sacc[rb][e0 + 1], sl2, -l2[rb][e0 >> 2][(e0 & 3) + 1]));
+          x[0] = fast_exp2(sacc[rb][e0] * sl2);
+          x[1] = fast_exp2(sacc[rb][e0 + 1] * sl2);
           uint32_t p2 = cvt_bf16x2(x);
           asm volatile("" : "+v"(p2));
           fw[2 * rb + (e0 >> 3)][(e0 & 7) >> 1] = p2;
@@ -385,7 +418,7 @@ dkv_kernel(BwdArgs a, int ktiles) {
         }
       }
     };
-    product_slots<NS + NKK * NDB, LA>(rd, mm, pre, work);
+    product_slots<NX + NS + NKK * NDB, LA>(rd, mm, pre, work);
   };
 
   using T_ = std::true_type;
@@ -707,7 +740,7 @@ hipError_t launch_bwd_t(const BwdArgs &a, hipStream_t stream) {
   const int64_t thr = pairs * (D / 8);
   hipLaunchKernelGGL((delta_kernel<D>), dim3((unsigned)((thr + 255) / 256)), dim3(256), 0,
                      stream, (const bf16_t *)a.o, (const bf16_t *)a.dout, a.lse, a.delta,
-                     a.lse2, a.total, a.hq);
+                     a.lse2, a.lsex, a.deltax, 1.f / a.scale, a.total, a.hq);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
 

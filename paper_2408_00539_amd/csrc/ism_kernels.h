@@ -128,6 +128,9 @@ struct BwdArgs {
   float *dq, *dk, *dv;
   float *delta;             // [hq, T] workspace: -rowsum(dO * O)
   float *lse2;              // [hq, T] workspace: lse * log2(e)
+  // [hq, 2, T] workspace: -lse / scale and -delta, each as the exact sum of
+  // three bf16 values (plane 0: the first two, plane 1: the third and zero)
+  uint32_t *lsex, *deltax;
   const int32_t *cu_seqlens;
   const int32_t *cu_segs;
   const uint8_t *seg_is_query;
