@@ -116,7 +116,6 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
       return align_up((size_t)total_tokens * 4);
     case ISM_OP_BWD:
       return 2 * align_up((size_t)total_tokens * 4) +
-             2 * align_up((size_t)total_tokens * hq * 4) +
              2 * align_up((size_t)total_tokens * hq * 8);
     case ISM_OP_PREFILL_CACHED:
       return 0;
@@ -200,9 +199,7 @@ extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
   const size_t tb = align_up((size_t)sg->total_tokens * 4);
   int32_t *lim = (int32_t *)ws;
   int32_t *seer = (int32_t *)((char *)ws + tb);
-  float *delta = (float *)((char *)ws + 2 * tb);
-  float *lse2 = (float *)((char *)delta + align_up((size_t)sg->total_tokens * hq * 4));
-  uint32_t *lsex = (uint32_t *)((char *)lse2 + align_up((size_t)sg->total_tokens * hq * 4));
+  uint32_t *lsex = (uint32_t *)((char *)ws + 2 * tb);
   uint32_t *deltax = (uint32_t *)((char *)lsex + align_up((size_t)sg->total_tokens * hq * 8));
   if ((st = hip_status(ism::launch_bwd_prep(sg->cu_segs, sg->seg_is_query, sg->num_segs,
                                             sg->total_tokens, lim, seer, s),
@@ -210,13 +207,12 @@ extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
     return st;
   ism::BwdArgs a{};
   a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse;
-  a.dq = dq; a.dk = dk; a.dv = dv; a.delta = delta; a.lse2 = lse2;
-  a.lsex = lsex; a.deltax = deltax;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.lsex = lsex; a.deltax = deltax;
   a.cu_seqlens = sg->cu_seqlens; a.cu_segs = sg->cu_segs;
   a.seg_is_query = sg->seg_is_query; a.lim = lim; a.seer = seer;
   a.batch = sg->batch; a.num_segs = sg->num_segs; a.hq = hq; a.hkv = hkv;
   a.total = sg->total_tokens; a.max_seqlen = sg->max_seqlen;
-  a.scale = scale; a.deterministic = deterministic;
+  a.scale = scale; a.inv_scale = 1.f / scale; a.deterministic = deterministic;
   const hipError_t e = ism::launch_bwd(a, d, s);
   if (e == hipErrorNotSupported)
     return fail(ISM_ERR_UNSUPPORTED, "backward configuration not supported");

@@ -6,19 +6,19 @@
 //     key i: the start of i's segment if it is a query segment, else i itself
 //     (every later row of the dialogue sees i as well, since lim is
 //     non-decreasing inside a dialogue and lim(j) >= j).
-//  2. delta[h][j] = sum_d dO[j,h,d] O[j,h,d]  (equals sum_i P_ji dP_ji),
-//     stored negated so that the dP accumulators start at -delta and
-//     dS = P o dP' needs no subtraction; for the dK/dV kernel -delta and
-//     -lse / scale are also stored as sums of three bf16 values, which one
-//     product per row block adds to every key of the block's rows.
+//  2. dQ kernel, row-tile outer like the forward (lane <-> row): forms its
+//     rows' delta[h][j] = sum_d dO[j,h,d] O[j,h,d] (equals sum_i P_ji dP_ji)
+//     in its prologue, recomputes S^T and dP^T per 64-key tile and
+//     accumulates dQ^T += K^T dS^T. It also stores -lse / scale and -delta
+//     of its rows as sums of three bf16 values for the dK/dV kernel, which
+//     runs next and adds them to every key of a row with one product per
+//     row block.
 //  3. dK/dV kernel, key-tile outer: a workgroup owns 128 keys of one KV head
 //     (32 per wave pair, lane <-> key), walks the query heads of the group
 //     and the 64-row tiles from seer[first key] to the dialogue end, and
 //     accumulates dV^T += dO^T P and dK^T += Q^T dS with P = exp(S - LSE),
 //     dS = P o (dP - delta), dP = dO V^T. Q and dO tiles are staged in LDS
 //     row-major; the products over rows read them through transposing reads.
-//  4. dQ kernel, row-tile outer like the forward (lane <-> row): recomputes
-//     S^T and dP^T per 64-key tile and accumulates dQ^T += K^T dS^T.
 // All products are bf16 MFMA 32x32x16 with fp32 accumulation; gradients are
 // written in fp32.
 #include "ism_common.h"
@@ -65,47 +65,6 @@ __device__ __forceinline__ void split3_bf16(float c, uint32_t &w0, uint32_t &w1)
   const float r2 = r1 - __uint_as_float(b1);
   w0 = (b0 >> 16) | b1;
   w1 = __float_as_uint(r2) >> 16;
-}
-
-// -delta over (row, head) pairs: D/8 lanes per pair, 16-byte loads; also the
-// LSE in log2 units (lse * log2 e) for the dQ kernel, and -lse / scale and
-// -delta split into bf16 summands for the dK/dV kernel, which adds them to
-// its S and dP accumulators with one product each.
-template <int D>
-__global__ void __launch_bounds__(256)
-delta_kernel(const bf16_t *__restrict__ o, const bf16_t *__restrict__ dout,
-             const float *__restrict__ lse, float *__restrict__ delta,
-             float *__restrict__ lse2, uint32_t *__restrict__ lsex,
-             uint32_t *__restrict__ deltax, float inv_scale, int32_t total, int32_t hq) {
-  constexpr int LPR = D / 8;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t pairs = (int64_t)total * hq;
-  const int64_t rh = min(gid / LPR, pairs - 1);
-  const int c = (int)(gid % LPR);
-  // read once: non-temporal loads keep them out of the caches
-  const u32x4 x = __builtin_nontemporal_load((const u32x4 *)(o + rh * D + c * 8));
-  const u32x4 y = __builtin_nontemporal_load((const u32x4 *)(dout + rh * D + c * 8));
-  float acc = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    acc = fmaf(bf16_lo(x[i]), bf16_lo(y[i]), acc);
-    acc = fmaf(bf16_hi(x[i]), bf16_hi(y[i]), acc);
-  }
-#pragma unroll
-  for (int s = 1; s < LPR; s <<= 1) acc += __shfl_xor(acc, s);
-  if (c == 0 && gid / LPR < pairs) {
-    const int64_t row = rh / hq, h = rh % hq;
-    const float l = lse[h * total + row];
-    delta[h * total + row] = -acc;
-    lse2[h * total + row] = l * kLog2e;
-    uint32_t w0, w1;
-    split3_bf16(-l * inv_scale, w0, w1);
-    lsex[2 * h * total + row] = w0;
-    lsex[(2 * h + 1) * total + row] = w1;
-    split3_bf16(-acc, w0, w1);
-    deltax[2 * h * total + row] = w0;
-    deltax[(2 * h + 1) * total + row] = w1;
-  }
 }
 
 // ---------------------------------------------------------------- dK / dV
@@ -567,18 +526,46 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
 
   const int rc = min(wq0 + l32, e - 1);
   const int lim_r = a.lim[rc];
-  const float lse2 = a.lse2[(int64_t)head * a.total + rc];
-  const float ndlt = a.delta[(int64_t)head * a.total + rc];  // -delta
+  const float lse_r = a.lse[(int64_t)head * a.total + rc];
   bf16x8 qf[NKS], df[NKS];
+  float ndlt;  // -delta of the lane's row
   {
-    const bf16_t *qp = (const bf16_t *)a.q + ((int64_t)rc * a.hq + head) * D + hf * 8;
-    const bf16_t *dp = (const bf16_t *)a.dout + ((int64_t)rc * a.hq + head) * D + hf * 8;
+    const int64_t ro = ((int64_t)rc * a.hq + head) * D + hf * 8;
+    const bf16_t *qp = (const bf16_t *)a.q + ro;
+    const bf16_t *dp = (const bf16_t *)a.dout + ro;
+    const bf16_t *opp = (const bf16_t *)a.o + ro;
+    bf16x8 of[NKS];
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       qf[ks] = *(const bf16x8 *)(qp + ks * 16);
       df[ks] = *(const bf16x8 *)(dp + ks * 16);
+      of[ks] = *(const bf16x8 *)(opp + ks * 16);
     }
     wait_loads();  // also drains the transfers above
+    // delta = rowsum(dO o O): this lane's half of the head dims, then the pair
+    float acc = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const u32x4 x = __builtin_bit_cast(u32x4, of[ks]), y = __builtin_bit_cast(u32x4, df[ks]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc = fmaf(bf16_lo(x[i]), bf16_lo(y[i]), acc);
+        acc = fmaf(bf16_hi(x[i]), bf16_hi(y[i]), acc);
+      }
+    }
+    ndlt = -pair_sum(acc);
+  }
+  const float lse2 = lse_r * kLog2e;
+  // -lse / scale and -delta of the row as bf16 summands for the dK/dV kernel
+  if (active && hf == 0 && wq0 + l32 < e) {
+    const int64_t i0 = 2 * (int64_t)head * a.total + wq0 + l32;
+    uint32_t w0, w1;
+    split3_bf16(-lse_r * a.inv_scale, w0, w1);
+    a.lsex[i0] = w0;
+    a.lsex[i0 + a.total] = w1;
+    split3_bf16(ndlt, w0, w1);
+    a.deltax[i0] = w0;
+    a.deltax[i0 + a.total] = w1;
   }
   __syncthreads();
   f32x16 dq[NDB];
@@ -734,22 +721,15 @@ hipError_t launch_dq(const BwdArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// dQ first: it also writes the per-row summands the dK/dV kernel reads.
 template <int D>
 hipError_t launch_bwd_t(const BwdArgs &a, hipStream_t stream) {
-  const int64_t pairs = (int64_t)a.total * a.hq;
-  const int64_t thr = pairs * (D / 8);
-  hipLaunchKernelGGL((delta_kernel<D>), dim3((unsigned)((thr + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t *)a.o, (const bf16_t *)a.dout, a.lse, a.delta,
-                     a.lse2, a.lsex, a.deltax, 1.f / a.scale, a.total, a.hq);
-  hipError_t err = hipGetLastError();
+  hipError_t err = launch_dq<D, 8>(a, stream);
   if (err != hipSuccess) return err;
-
   const int ktiles = (a.max_seqlen + kKW - 1) / kKW;
   hipLaunchKernelGGL((dkv_kernel<D>), dim3((unsigned)xcd_grid((int64_t)a.batch * a.hkv, ktiles)),
                      dim3(512), 0, stream, a, ktiles);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
-
-  return launch_dq<D, 8>(a, stream);
+  return hipGetLastError();
 }
 
 }  // namespace

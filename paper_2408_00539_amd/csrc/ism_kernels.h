@@ -126,10 +126,9 @@ struct BwdArgs {
   const void *q, *k, *v, *o, *dout;
   const float *lse;
   float *dq, *dk, *dv;
-  float *delta;             // [hq, T] workspace: -rowsum(dO * O)
-  float *lse2;              // [hq, T] workspace: lse * log2(e)
-  // [hq, 2, T] workspace: -lse / scale and -delta, each as the exact sum of
-  // three bf16 values (plane 0: the first two, plane 1: the third and zero)
+  // [hq, 2, T] workspace, written by the dQ kernel for the dK/dV kernel:
+  // -lse / scale and -delta (delta = rowsum(dO * O)), each as the exact sum
+  // of three bf16 values (plane 0: the first two, plane 1: the third and 0)
   uint32_t *lsex, *deltax;
   const int32_t *cu_seqlens;
   const int32_t *cu_segs;
@@ -137,7 +136,7 @@ struct BwdArgs {
   const int32_t *lim;       // [T] inclusive key bound per row
   const int32_t *seer;      // [T] first row that sees each key
   int32_t batch, num_segs, hq, hkv, total, max_seqlen;
-  float scale;
+  float scale, inv_scale;
   int32_t deterministic;
 };
 
