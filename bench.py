@@ -1,7 +1,7 @@
 """Benchmark of the ISM attention hot path on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                [--only all|step|gqa|bwd|cache|expansion|latency]
+                [--only all|step|gqa|bwd|cache|expansion|latency|decode_groups]
                 [--calibrate-copy]
 
 A step is one training pass of the attention hot path over one batch of
@@ -18,7 +18,8 @@ The other paths are measured on their own workloads and reported under
 ``paths``: the forward and the training step of workload 1 (8 x 4096), the
 grouped-KV forward (workload 2, 2 x 16384, 32/8 heads), the cached prefill and the decode stream (workload
 3, dense and paged, with draft verification, 2-D positions and the measured
-streaming-read ceiling).
+streaming-read ceiling), and the decode step with 1, 4, 6 and 8 query heads
+per KV head (32 dialogues at position 8192, 8 KV heads).
 
 Two comparisons from the paper ride along under ``paths``: the training cost
 of the prefix mask's sample expansion against ISM's single pass over the same
@@ -32,7 +33,7 @@ backward of some (dialogue, head) pairs) as the headline figure, and the
 forwards of workloads 1 and 2 and the cache path of workload 3 (one-shot
 reference rows, then 16 stepwise decode steps) beside it.
 
-``--only gqa|bwd|cache|expansion|latency`` measures that one path alone (for
+``--only gqa|bwd|cache|expansion|latency|decode_groups`` measures that one path alone (for
 per-kernel profiles of one workload) and prints a JSON line with ``paths``
 only; ``--only step`` runs the headline step alone.
 
@@ -464,6 +465,41 @@ def bench_latency(timer, reps=5, seed=5):
     return {"latency": res}
 
 
+DG_B, DG_POS, DG_CAP, DG_HKV, DG_D = 32, 8192, 9216, 8, 128
+DG_HQ = (8, 32, 48, 64)  # query heads per KV head: 1, 4, 6, 8
+
+
+def bench_decode_groups(timer, reps=50, seed=6):
+    """The decode step with grouped KV heads: 32 dialogues at position 8192
+    (cache capacity 9216), 8 KV heads of 128, and 8, 32, 48 or 64 query
+    heads (1, 4, 6 or 8 per KV head). Bytes per step: K and V of every key
+    once, whatever the grouping (a workgroup serves all query heads of its
+    KV head, up to 8). Inputs: seeded N(0, 1) bf16 drawn on the device."""
+    from paper_2408_00539_amd import ops
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+
+    def rnd(*shape):
+        return torch.randn(*shape, generator=g, device="cuda",
+                           dtype=torch.float32).to(torch.bfloat16)
+    kc, vc = rnd(DG_B, DG_HKV, DG_CAP, DG_D), rnd(DG_B, DG_HKV, DG_CAP, DG_D)
+    kn, vn = rnd(DG_B, DG_HKV, DG_D), rnd(DG_B, DG_HKV, DG_D)
+    lens = torch.full((DG_B,), DG_POS, dtype=torch.int32, device="cuda")
+    nbytes = DG_B * DG_HKV * 2 * (DG_POS + 1) * DG_D * 2
+    res = {"workload": f"{DG_B} dialogues at position {DG_POS}, {DG_HKV} KV heads, "
+                       f"head_dim {DG_D}", "bytes_per_step": nbytes}
+    for hq in DG_HQ:
+        q = rnd(DG_B, hq, DG_D)
+        # (a repeated step writes the same key to the same position)
+        ms = timer.run(lambda: ops.decode(q, kn, vn, kc, vc, lens), reps, 5, WARM_MS)
+        res[f"g{hq // DG_HKV}"] = {"hq": hq, "ms_per_step": round(ms, 4),
+                                   "gbs": round(nbytes / ms / 1e6, 1),
+                                   "frac_peak_hbm": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+    del kc, vc
+    return {"decode_head_groups": res}
+
+
 def _f64(bits):
     from paper_2408_00539_amd.workloads import bf16_bits_to_f32
     return bf16_bits_to_f32(bits).astype(np.float64)
@@ -736,7 +772,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["all", "step", "gqa", "bwd", "cache",
-                                       "expansion", "latency"],
+                                       "expansion", "latency", "decode_groups"],
                     default="all")
     ap.add_argument("--calibrate-copy", action="store_true")
     ap.add_argument("--write-traffic-record", nargs="+", metavar="CSV",
@@ -764,7 +800,7 @@ def main():
         calibrate_copy()
         return
     timer = Timer()
-    if args.only in ("gqa", "bwd", "cache", "expansion", "latency"):
+    if args.only in ("gqa", "bwd", "cache", "expansion", "latency", "decode_groups"):
         paths = {}
         if args.only == "gqa":
             w2 = W.make_workload(2)
@@ -781,6 +817,8 @@ def main():
             w1.do = W.packed_tensor(w1.seed, W.DO, w1.segs.cu_seqlens, w1.hq, w1.d)
             tr = bench_training(w1, timer, 5, 1, True)
             paths.update(bench_expansion(w1, timer, 3, 1, tr["step"]["ms"]))
+        elif args.only == "decode_groups":
+            paths.update(bench_decode_groups(timer))
         else:
             paths.update(bench_latency(timer))
         print(json.dumps({"paths": paths}), flush=True)
@@ -818,6 +856,9 @@ def main():
         torch.cuda.empty_cache()
         log("latency turns ...")
         paths.update(bench_latency(timer))
+        torch.cuda.empty_cache()
+        log("decode with grouped KV heads ...")
+        paths.update(bench_decode_groups(timer))
         torch.cuda.empty_cache()
 
     cpu = None

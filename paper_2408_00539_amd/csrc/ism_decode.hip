@@ -62,6 +62,26 @@ cache_append_paged_kernel(const bf16_t *__restrict__ k_src, const bf16_t *__rest
   *(u32x4 *)(v_pages + dst) = *(const u32x4 *)(v_src + src);
 }
 
+// Sum of x over each group of N (8 or 16) consecutive lanes, in every lane
+// of the group, through DPP lane moves (no LDS round trip, unlike a
+// shuffle): quad xor 1, quad xor 2, the mirror inside each 8-lane half row,
+// and for N = 16 the mirror inside the 16-lane row. Each step adds two values
+// that are uniform over their subgroups, so all lanes end with the same bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(N == 8 || N == 16, "groups of 8 or 16 lanes");
+  x += dpp_move<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+  x += dpp_move<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+  x += dpp_move<0x141>(x);  // row_half_mirror
+  if constexpr (N == 16) x += dpp_move<0x140>(x);  // row_mirror
+  return x;
+}
+
 // Split decode step. Each dialogue's key range [0, p] is cut into a.splits
 // chunks of equal length rounded up to a whole workgroup iteration (4 KPW
 // keys), so every chunk but the last runs whole iterations and the longest
@@ -79,7 +99,7 @@ __global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
   constexpr int CPK = D / 8;     // lanes per key row (16 bytes each)
   constexpr int KPI = 64 / CPK;  // keys per wave-wide load
-  constexpr int U = 8;           // loads in flight per lane per tensor
+  constexpr int U = GS > 4 ? 4 : 8;  // loads in flight per lane per tensor
   constexpr int KPW = U * KPI;   // keys per wave per iteration
   __shared__ float sm_o[4][GS][D];
   __shared__ float sm_m[4][GS], sm_l[4][GS];
@@ -173,8 +193,7 @@ decode_split_kernel(DecodeArgs a) {
           acc = fmaf(qv[g][2 * i], bf16_lo(kr[u][i]), acc);
           acc = fmaf(qv[g][2 * i + 1], bf16_hi(kr[u][i]), acc);
         }
-#pragma unroll
-        for (int x = 1; x < CPK; x <<= 1) acc += __shfl_xor(acc, x);
+        acc = group_sum<CPK>(acc);
         s[u] = (base + u * KPI + slot < k1) ? acc : -INFINITY;
         mt = fmaxf(mt, s[u]);
       }
