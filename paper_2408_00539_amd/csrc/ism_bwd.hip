@@ -556,6 +556,14 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
     ndlt = -pair_sum(acc);
   }
   const float lse2 = lse_r * kLog2e;
+  // -delta of the row as bf16 summands: for the dK/dV kernel and, as the B
+  // operand of one product per key half against a ones A operand (1 in k
+  // slots 0-2 of lanes 0-31), to start the dP^T accumulators at -delta
+  uint32_t dw0, dw1;
+  split3_bf16(ndlt, dw0, dw1);
+  const bf16x8 dsum = __builtin_bit_cast(bf16x8, u32x4{dw0, dw1, 0u, 0u});
+  const bf16x8 ones3 = __builtin_bit_cast(
+      bf16x8, hf ? u32x4{0u, 0u, 0u, 0u} : u32x4{0x3f803f80u, 0x3f80u, 0u, 0u});
   // -lse / scale and -delta of the row as bf16 summands for the dK/dV kernel
   if (active && hf == 0 && wq0 + l32 < e) {
     const int64_t i0 = 2 * (int64_t)head * a.total + wq0 + l32;
@@ -563,9 +571,8 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
     split3_bf16(-lse_r * a.inv_scale, w0, w1);
     a.lsex[i0] = w0;
     a.lsex[i0 + a.total] = w1;
-    split3_bf16(ndlt, w0, w1);
-    a.deltax[i0] = w0;
-    a.deltax[i0 + a.total] = w1;
+    a.deltax[i0] = dw0;
+    a.deltax[i0 + a.total] = dw1;
   }
   __syncthreads();
   f32x16 dq[NDB];
@@ -604,11 +611,14 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       f32x16 sc[2], pc[2];
       u32x4 ds[2][2];
       constexpr int NH = 2 * NKS;  // products per half (S^T and dP^T)
-      // products: [0, NH) S^T and dP^T half 0 (alternating), [NH, 2 NH) half 1,
-      // [2 NH, 2 NH + 4 NDB) dQ^T (kb, db, bt)
+      constexpr int NX = 2;        // the two -delta products come first
+      // products after those (index n - NX): [0, NH) S^T and dP^T half 0
+      // (alternating), [NH, 2 NH) half 1, [2 NH, 2 NH + 4 NDB) dQ^T (kb, db, bt)
       auto rd = [&](auto nc) __attribute__((always_inline)) -> bf16x8 {
-        constexpr int n = decltype(nc)::value;
-        if constexpr (n < 2 * NH) {
+        constexpr int n = decltype(nc)::value - NX;
+        if constexpr (n < 0) {
+          return ones3;
+        } else if constexpr (n < 2 * NH) {
           constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
           return *(const bf16x8 *)(((m & 1) ? vl : kl) + kb * 32 * RB + so.row(ks));
         } else {
@@ -619,10 +629,12 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
         }
       };
       auto mm = [&](auto nc, bf16x8 x) __attribute__((always_inline)) {
-        constexpr int n = decltype(nc)::value;
-        if constexpr (n < 2 * NH) {
+        constexpr int n = decltype(nc)::value - NX;
+        if constexpr (n < 0) {
+          pc[n + NX] = mfma32x32x16(x, dsum, f32x16{});
+        } else if constexpr (n < 2 * NH) {
           constexpr int kb = n / NH, m = n % NH, ks = m >> 1;
-          if constexpr (m & 1) pc[kb] = mfma32x32x16(x, df[ks], ks == 0 ? f32x16{} : pc[kb]);
+          if constexpr (m & 1) pc[kb] = mfma32x32x16(x, df[ks], pc[kb]);
           else sc[kb] = mfma32x32x16(x, qf[ks], ks == 0 ? f32x16{} : sc[kb]);
         } else {
           constexpr int j = n - 2 * NH, kb = j / (2 * NDB), db = (j % (2 * NDB)) >> 1,
@@ -632,7 +644,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       };
       // mask a finished S^T half just before its exponentials start
       auto pre = [&](auto nc) __attribute__((always_inline)) {
-        constexpr int n = decltype(nc)::value;
+        constexpr int n = decltype(nc)::value - NX;
         if constexpr (n == NH) { if (!full) mask(sc[0], c0); }
         if constexpr (n == 2 * NH) { if (!full) mask(sc[1], c0 + 32); }
       };
@@ -649,14 +661,14 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
       };
       auto ds2 = [&](int kb, int r) __attribute__((always_inline)) {  // elements r, r + 1 (r even)
         f32x2 x;
-        x[0] = sc[kb][r] * (pc[kb][r] + ndlt);
-        x[1] = sc[kb][r + 1] * (pc[kb][r + 1] + ndlt);
+        x[0] = sc[kb][r] * pc[kb][r];
+        x[1] = sc[kb][r + 1] * pc[kb][r + 1];
         uint32_t w = cvt_bf16x2(x);
         asm volatile("" : "+v"(w));
         ds[kb][r >> 3][(r & 7) >> 1] = w;
       };
       auto work = [&](auto nc) __attribute__((always_inline)) {
-        constexpr int n = decltype(nc)::value;
+        constexpr int n = decltype(nc)::value - NX;
         if constexpr (n >= NH && n < 2 * NH) {
           constexpr int E = 32 / NH, w = n - NH;  // element-steps per slot
           if constexpr (w < NH / 2) {
@@ -677,7 +689,7 @@ dq_kernel(BwdArgs a, int hpw, int tiles) {
           }
         }
       };
-      product_slots<2 * NH + 4 * NDB, LA>(rd, mm, pre, work);
+      product_slots<NX + 2 * NH + 4 * NDB, LA>(rd, mm, pre, work);
     }
     wait_vmem();
     __syncthreads();
