@@ -719,7 +719,7 @@ def write_traffic_record(fetch_copy, fetch_step, write_copy, write_step,
                                  "bytes": int(sf * f * 1024 + sw * w * 1024)}
     kb = rec["kernels"]
     rec["bwd_bytes_per_launch"] = sum(
-        kb[k]["bytes"] for k in kb if k.startswith(("delta_kernel", "dkv_kernel", "dq_kernel")))
+        kb[k]["bytes"] for k in kb if k.startswith(("bwd_prep_kernel", "dkv_kernel", "dq_kernel")))
     rec["fwd_bytes_per_launch"] = sum(
         kb[k]["bytes"] for k in kb if k.startswith("fwd_kernel<128, false"))
     dec = [k for k in kb if k.startswith("decode_split_kernel")]
