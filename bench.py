@@ -785,7 +785,7 @@ def main():
         write_traffic_record(*args.write_traffic_record)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU "
+        print("bench.py measures one GPU only: this library has no multi-GPU "
               "path (see the sharding design); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)

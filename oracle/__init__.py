@@ -8,7 +8,7 @@ code with the HIP library or its Python binding, and imports neither.
 Every function here is written from the paper (arXiv 2408.00539,
 "Intermittent Semi-working Mask: A New Masking Paradigm for LLMs"):
 the visibility bound f(j) of Eq. 5, the masked attention update of Eq. 4 in
-its softmax form (Sec. 2.3, "Practical Integration"), the KV-cache reuse
+its softmax form (Sec. 2.3, on integrating the mask), the KV-cache reuse
 procedure of Sec. 2.3, and ChatGLM-style 2-D rotary positions (the
 prefix-backbone adaptation of Sec. 2.3, module ``rope2d``).
 """
