@@ -1,0 +1,136 @@
+"""Index range: tensors of more than 2^31 elements.
+
+Offsets into q/o (forward) and into the KV cache (decode) pass 2^31
+elements here, so any 32-bit offset arithmetic in the kernels would read or
+write the wrong rows. Queries are zero, so each output is a closed form of
+the oracle (uniform weights over the visible keys, Eq. 5) and the values
+themselves need no dense reference: the forward over 5 dialogues of 65536
+tokens with 64 query heads on one KV head (q and o 2.7e9 elements each),
+and a decode step over a 24 x 8 x 131072-position cache (K and V 3.2e9
+elements each). Inputs are seeded normal values drawn on the device; the
+expected values are computed by the oracle on the host from a copy.
+Outputs are filled with NaN before the launch.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2408_00539_amd import workloads as W
+from tests._closed_form import LSE_TOL, O_ABS, O_REL
+from tests._gpu import announce, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _layout(rng, n_dialogues, length):
+    """Dialogues of exactly `length` tokens alternating query segments of
+    64-2048 tokens and answer segments of 256-8192 tokens."""
+    dias = []
+    for _ in range(n_dialogues):
+        parts, left, q = [], length, True
+        while left:
+            hi = 2048 if q else 8192
+            ln = min(left, int(rng.integers(64 if q else 256, hi + 1)))
+            parts.append((ln, q))
+            left -= ln
+            q = not q
+        dias.append(parts)
+    return W.segments_from_lengths(dias)
+
+
+def _check_rows(torch, name, got, ref):
+    """|got - ref| <= O_REL |ref| + O_ABS on every element, on the device
+    (got bf16 [T, d] view, ref fp32 [T, d]); got must be finite."""
+    g = got.float()
+    assert bool(torch.isfinite(g).all()), f"{name}: non-finite values"
+    bad = (g - ref).abs() > O_REL * ref.abs() + O_ABS
+    nbad = int(bad.sum())
+    err = float((g - ref).abs().max())
+    print(f"{name}: max abs err {err:.3e}, {nbad} elements over the bar")
+    assert nbad == 0, f"{name}: {nbad} elements over the bar (max abs err {err:.3e})"
+
+
+@pytest.mark.timeout(900)
+def test_fwd_beyond_2_31_elements():
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    B, L, hq, hkv, d = 5, 65536, 64, 1, 128
+    segs = _layout(np.random.default_rng(20), B, L)
+    T = segs.total
+    assert T * hq * d > 2 ** 31
+    announce("fwd index range", T, hq, hkv, d)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(20)
+    k = torch.randn((T, hkv, d), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((T, hkv, d), generator=g, device="cuda").to(torch.bfloat16)
+    q = torch.zeros((T, hq, d), dtype=torch.bfloat16, device="cuda")
+    o = torch.full((T, hq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((hq, T), float("nan"), dtype=torch.float32, device="cuda")
+    dsegs = ops.Segments.from_host(segs.cu_seqlens, segs.cu_segs, segs.seg_is_query)
+    ops.fwd(q, k, v, dsegs, d ** -0.5, out=(o, lse))
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.uniform_fwd(v.float().cpu().numpy(), segs.cu_seqlens,
+                                        segs.cu_segs, segs.seg_is_query)
+    ref = torch.from_numpy(o_ref[:, 0].astype(np.float32)).cuda()
+    lref = torch.from_numpy(lse_ref.astype(np.float32)).cuda()
+    lerr = float((lse.double() - lref.double()[None, :]).abs().max())
+    print(f"LSE: max abs err {lerr:.3e} (bar {LSE_TOL})")
+    assert lerr <= LSE_TOL
+    # the heads at both ends and the middle, and the last rows of every head
+    for h in (0, 1, hq // 2, hq - 1):
+        _check_rows(torch, f"O h{h}", o[:, h], ref)
+    tail = o[T - 4096:].float()
+    assert bool(torch.isfinite(tail).all())
+    terr = (tail - ref[T - 4096:, None, :]).abs()
+    assert bool((terr <= O_REL * ref[T - 4096:, None, :].abs() + O_ABS).all()), \
+        f"O last rows, all heads: max abs err {float(terr.max()):.3e}"
+    del q, o, lse, k, v, ref
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_decode_beyond_2_31_elements():
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    B, hkv, hq, d, cap = 24, 8, 32, 128, 131072
+    assert B * hkv * cap * d > 2 ** 31
+    announce("decode index range", B, hkv, hq, cap, d)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(21)
+    # zero keys and queries: every score is 0, the output is the mean of V
+    kc = torch.zeros((B, hkv, cap, d), dtype=torch.bfloat16, device="cuda")
+    vc = torch.randn((B, hkv, cap, d), generator=g, device="cuda").to(torch.bfloat16)
+    kn = torch.zeros((B, hkv, d), dtype=torch.bfloat16, device="cuda")
+    vn = torch.randn((B, hkv, d), generator=g, device="cuda").to(torch.bfloat16)
+    q = torch.zeros((B, hq, d), dtype=torch.bfloat16, device="cuda")
+    # positions near the end of the slabs, one per dialogue
+    pos = np.array([cap - 1 - 977 * b for b in range(B)], dtype=np.int32)
+    lens = torch.from_numpy(pos).cuda()
+    o = torch.full((B, hq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((hq, B), float("nan"), dtype=torch.float32, device="cuda")
+    ops.decode(q, kn, vn, kc, vc, lens, 0, d ** -0.5, out=(o, lse))
+    torch.cuda.synchronize()
+    # the new value must sit at its position now
+    for b in (0, B - 1):
+        p = int(pos[b])
+        assert bool(torch.equal(vc[b, :, p], vn[b])), b
+    G = hq // hkv
+    o_h, lse_h = o.float().cpu().numpy(), lse.cpu().numpy()
+    for b in range(B):
+        p = int(pos[b])
+        lref = np.log(p + 1.0)
+        assert np.max(np.abs(lse_h[:, b] - lref)) <= LSE_TOL, b
+        for h in range(hkv):
+            vals = vc[b, h, :p + 1].float().cpu().numpy()
+            # the oracle's closed form for one query row that sees keys 0..p
+            ref, _ = oracle.uniform_fwd(vals[:, None, :], np.array([0, p + 1], np.int32),
+                                        np.array([0, p + 1], np.int32), np.ones(1, np.uint8))
+            ref = ref[-1, 0]
+            got = o_h[b, h * G:(h + 1) * G]
+            assert np.all(np.isfinite(got)), (b, h)
+            err = np.abs(got - ref[None, :])
+            assert np.all(err <= O_REL * np.abs(ref)[None, :] + O_ABS), \
+                f"decode b{b} kv head {h}: max abs err {err.max():.3e}"
+    del kc, vc, q, o, lse
+    torch.cuda.empty_cache()
