@@ -4,9 +4,9 @@ Offsets into q/o (forward) and into the KV cache (decode) pass 2^31
 elements here, so any 32-bit offset arithmetic in the kernels would read or
 write the wrong rows. Queries are zero, so each output is a closed form of
 the oracle (uniform weights over the visible keys, Eq. 5) and the values
-themselves need no dense reference: the forward over 5 dialogues of 65536
-tokens with 64 query heads on one KV head (q and o 2.7e9 elements each),
-and a decode step over a 24 x 8 x 131072-position cache (K and V 3.2e9
+themselves need no dense reference: the forward and the backward (dO = 1)
+over 5 dialogues of 65536 tokens with 64 query heads on one KV head (q,
+o, dO 2.7e9 elements each, dQ in fp32), and a decode step over a 24 x 8 x 131072-position cache (K and V 3.2e9
 elements each). Inputs are seeded normal values drawn on the device; the
 expected values are computed by the oracle on the host from a copy.
 Outputs are filled with NaN before the launch.
@@ -17,8 +17,8 @@ import pytest
 
 import oracle
 from paper_2408_00539_amd import workloads as W
-from tests._closed_form import LSE_TOL, O_ABS, O_REL
-from tests._gpu import announce, torch_cuda
+from tests._closed_form import LSE_TOL, O_ABS, O_REL, bf16_round
+from tests._gpu import MAX_ABS, MEAN_ABS, announce, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -86,6 +86,65 @@ def test_fwd_beyond_2_31_elements():
     assert bool((terr <= O_REL * ref[T - 4096:, None, :].abs() + O_ABS).all()), \
         f"O last rows, all heads: max abs err {float(terr.max()):.3e}"
     del q, o, lse, k, v, ref
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_bwd_beyond_2_31_elements():
+    """One KV head and dO = 1: every query head has the same dQ (the
+    oracle's single-head closed form), dK = 0 exactly and dV is the sum of
+    the 64 heads' equal contributions."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    B, L, hq, hkv, d = 5, 65536, 64, 1, 128
+    segs = _layout(np.random.default_rng(22), B, L)
+    T = segs.total
+    assert T * hq * d > 2 ** 31
+    announce("bwd index range", T, hq, hkv, d)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(22)
+    k = torch.randn((T, hkv, d), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((T, hkv, d), generator=g, device="cuda").to(torch.bfloat16)
+    q = torch.zeros((T, hq, d), dtype=torch.bfloat16, device="cuda")
+    dsegs = ops.Segments.from_host(segs.cu_seqlens, segs.cu_segs, segs.seg_is_query)
+    scale = d ** -0.5
+    o, lse = ops.fwd(q, k, v, dsegs, scale)
+    do = torch.ones_like(q)
+    dq = torch.full((T, hq, d), float("nan"), dtype=torch.float32, device="cuda")
+    dk = torch.full((T, hkv, d), float("nan"), dtype=torch.float32, device="cuda")
+    dv = torch.full((T, hkv, d), float("nan"), dtype=torch.float32, device="cuda")
+    ops.bwd(q, k, v, o, lse, do, dsegs, scale, out=(dq, dk, dv))
+    torch.cuda.synchronize()
+    del o, do
+    args = (segs.cu_seqlens, segs.cu_segs, segs.seg_is_query)
+    L_ = oracle.lim(*args)
+    n = L_ - segs.cu_seqlens[oracle.seq_index(segs.cu_seqlens, T)] + 1
+    rq, _, rv = oracle.uniform_bwd(k.float().cpu().numpy(), v.float().cpu().numpy(), 1,
+                                   scale, *args, row_weight=bf16_round(1.0 / n))
+    assert bool(torch.isfinite(dk).all()) and int(torch.count_nonzero(dk)) == 0
+    ref_q = torch.from_numpy(rq[:, 0].astype(np.float32)).cuda()
+    for h in (0, 1, hq // 2, hq - 1):
+        gq = dq[:, h]
+        assert bool(torch.isfinite(gq).all()), h
+        err = (gq - ref_q).abs()
+        mx, mn = float(err.max()), float(err.mean())
+        print(f"dQ h{h}: max abs {mx:.3e}, mean abs {mn:.3e}")
+        assert mx <= MAX_ABS and mn <= MEAN_ABS, h
+    tail = dq[T - 4096:]
+    assert bool(torch.isfinite(tail).all())
+    assert float((tail - ref_q[T - 4096:, None, :]).abs().max()) <= MAX_ABS
+    # dV_i sums 64 heads x up to 65536 rows of weights ~1 / n (values up
+    # to ~700) in fp32: some 2.6e5 additions of ~1e-4 each round at ~3e-5
+    # against the fp64 oracle, so the bound is relative; a wrong row or key
+    # range would be off by whole weights per row
+    ref_v = torch.from_numpy((hq * rv[:, 0]).astype(np.float32)).cuda()
+    assert bool(torch.isfinite(dv).all())
+    err = (dv[:, 0] - ref_v).abs()
+    rel = float((err / ref_v.abs().clamp_min(1.0)).max())
+    print(f"dV: max abs {float(err.max()):.3e}, mean abs {float(err.mean()):.3e}, "
+          f"max relative {rel:.3e}")
+    assert bool((err <= 2e-3 * ref_v.abs() + MAX_ABS).all())
+    del q, dq, dk, dv, k, v, ref_q, ref_v, tail
     torch.cuda.empty_cache()
 
 
