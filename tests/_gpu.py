@@ -47,7 +47,12 @@ def compare(name, got, ref, max_abs=MAX_ABS, mean_abs=MEAN_ABS, where=None):
     assert np.all(np.isfinite(got[m])), f"{name}: non-finite GPU values"
     mx, mn = float(err.max()), float(err.mean())
     msg = f"{name}: max abs {mx:.3e} (bar {max_abs}), mean abs {mn:.3e} (bar {mean_abs})"
-    print(msg)
+    # also reported: the largest |ref|, and the error in units of the bf16
+    # spacing at each reference value (2^(e - 7) for |ref| in [2^e, 2^(e+1)),
+    # references below 1e-6 counted at 1e-6)
+    r = np.abs(ref[m])
+    ulp = np.exp2(np.floor(np.log2(np.maximum(r, 1e-6))) - 7)
+    print(f"{msg}; max |ref| {float(r.max()):.3e}, max err {float((err / ulp).max()):.2f} bf16 ulps")
     sys.stdout.flush()
     assert mx <= max_abs and mn <= mean_abs, msg
     return mx, mn
