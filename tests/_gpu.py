@@ -47,12 +47,19 @@ def compare(name, got, ref, max_abs=MAX_ABS, mean_abs=MEAN_ABS, where=None):
     assert np.all(np.isfinite(got[m])), f"{name}: non-finite GPU values"
     mx, mn = float(err.max()), float(err.mean())
     msg = f"{name}: max abs {mx:.3e} (bar {max_abs}), mean abs {mn:.3e} (bar {mean_abs})"
-    # also reported: the largest |ref|, and the error in units of the bf16
-    # spacing at each reference value (2^(e - 7) for |ref| in [2^e, 2^(e+1)),
-    # references below 1e-6 counted at 1e-6)
+    # also reported: the largest |ref| and, for the bf16 output O, the error
+    # in units of the bf16 spacing (2^(e - 7) for |x| in [2^e, 2^(e+1))): the
+    # largest error against the spacing at the tensor's largest |ref|, and the
+    # median error against the spacing at each element's own |ref|
     r = np.abs(ref[m])
-    ulp = np.exp2(np.floor(np.log2(np.maximum(r, 1e-6))) - 7)
-    print(f"{msg}; max |ref| {float(r.max()):.3e}, max err {float((err / ulp).max()):.2f} bf16 ulps")
+    rmax = float(r.max())
+    extra = f"; max |ref| {rmax:.3e}"
+    if name.startswith("O") and rmax > 0:
+        spacing = lambda x: np.exp2(np.floor(np.log2(x)) - 7)
+        per_elem = err / spacing(np.maximum(r, 2.0 ** -40))
+        extra += (f", max err {mx / float(spacing(rmax)):.2f} bf16 ulps at that scale,"
+                  f" median {float(np.median(per_elem)):.2f} ulps per element")
+    print(msg + extra)
     sys.stdout.flush()
     assert mx <= max_abs and mn <= mean_abs, msg
     return mx, mn
