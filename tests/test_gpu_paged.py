@@ -51,7 +51,7 @@ def _gather_dense(pool, table):
 
 @pytest.mark.parametrize("page_size", [64, 128])
 @pytest.mark.parametrize("hq,hkv,d", [(4, 4, 128), (8, 2, 128), (4, 1, 64), (4, 2, 64),
-                                      (8, 1, 128)])
+                                      (8, 1, 128), (8, 1, 64)])
 @pytest.mark.parametrize("seg_is_query", [True, False])
 def test_paged_turn_matches_dense_and_oracle(page_size, hq, hkv, d, seg_is_query):
     torch = torch_cuda()
