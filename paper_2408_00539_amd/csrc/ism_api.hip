@@ -92,12 +92,16 @@ ism_status hip_status(hipError_t e, const char *what) {
 
 // Split count of a decode step; `sets` = head sets per dialogue (hkv when
 // hq / hkv <= 8).
-int decode_splits(int32_t batch, int32_t sets, int32_t max_len, int32_t req) {
+int decode_splits(int32_t batch, int32_t sets, int32_t max_len, int32_t req, bool mma) {
   if (req > 0) return req;
-  // about 2048 workgroups (two rounds of four per CU), at least 256 keys
-  // per chunk, at most 64 chunks
+  // about 2048 four-wave workgroups (two rounds of four per CU) for the
+  // vector kernel; about 768 one-wave workgroups (three per CU) for the
+  // matrix-core kernel, whose long chunks stream faster (on 256 slabs of 8192
+  // keys: 6.2 TB/s dense and 6.4 paged, against 5.5 and 5.5 with 4096 and
+  // 6.1 and 6.3 with 1024); at least 256 keys per chunk, at most 64 chunks
   const int slabs = batch * sets;
-  int s = (2048 + slabs - 1) / slabs;
+  const int target = mma ? 768 : 2048;
+  int s = (target + slabs - 1) / slabs;
   const int by_len = (max_len + 255) / 256;
   if (s > by_len) s = by_len;
   if (s > 64) s = 64;
@@ -122,7 +126,8 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
     case ISM_OP_DECODE: {
       if (hkv < 1 || hq < hkv || hq % hkv) return 0;
       const int sets = hq / ism::decode_heads_per_set(hq, hkv);
-      const size_t s = (size_t)decode_splits(batch, sets, max_seqlen, num_splits);
+      const size_t s = (size_t)decode_splits(batch, sets, max_seqlen, num_splits,
+                                             ism::decode_mma_heads(hq, hkv) > 0);
       return align_up((size_t)batch * hq * s * d * 4) +
              align_up((size_t)batch * hq * s * 2 * 4);
     }
@@ -431,8 +436,9 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
                 cache_cap);
   if (num_splits < 0 || num_splits > 1024)
     return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
-  const int splits =
-      decode_splits(batch, hq / ism::decode_heads_per_set(hq, hkv), max_seqlen, num_splits);
+  const int set_heads = ism::decode_heads_per_set(hq, hkv);
+  const bool mma = ism::decode_mma_heads(hq, hkv) > 0;
+  const int splits = decode_splits(batch, hq / set_heads, max_seqlen, num_splits, mma);
   const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen, hq,
                                               hkv, d, num_splits);
   if ((st = check_ws(ws, ws_bytes, need))) return st;
@@ -447,6 +453,8 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
   a.batch = batch; a.hq = hq; a.hkv = hkv; a.cap = cache_cap;
   a.splits = splits;
   a.scale = scale;
+  a.set_heads = set_heads;
+  a.mma = mma ? 1 : 0;
   if (pg) {
     a.block_table = pg->block_table;
     a.max_pages = pg->max_pages;

@@ -128,11 +128,19 @@ __device__ __forceinline__ void dma_x4(const void *g, uint32_t lds_base) {
 // The same with a wave-uniform base address in SGPRs and a per-lane 32-bit
 // byte offset (the address is base + offset): no 64-bit address arithmetic
 // per transfer.
+// NT: a non-temporal load (data read once, such as a KV-cache stream).
+template <bool NT = false>
 __device__ __forceinline__ void dma_x4s(const void *base, uint32_t off, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_base))
-               : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+                 :
+                 : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory", "m0");
 }
 __device__ __forceinline__ void dma_x1(const void *g, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off"
@@ -159,14 +167,21 @@ __device__ __forceinline__ void wait_loads() {
 // Wait until this wave's outstanding vector-memory operations, including
 // global->LDS transfers, have completed.
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// The same, leaving the wave's N most recent vector-memory operations in
+// flight (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vmem_but() {
+  static_assert(N >= 0 && N < 64, "vmcnt takes 0..63");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 // Direct global->LDS staging of a ROWS x D bf16 tile (unpadded, swizzled)
 // by the NW waves of a workgroup. Each global_load_lds_dwordx4 writes lane
 // l's 16 bytes to LDS bytes [16 l, 16 l + 16) of a 1 KB block, so the swizzle
 // is applied by choosing each lane's source chunk. No registers hold the
 // data. Block q of the tile is issued by wave q % NW; the workgroup has
-// exactly NW waves.
-template <int D, int ROWS, int NW = 4>
+// exactly NW waves. NT: non-temporal transfers (see dma_x4s).
+template <int D, int ROWS, int NW = 4, bool NT = false>
 struct DmaTile {
   static constexpr int CPR = D / 8;                 // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;              // rows per 1 KB transfer
@@ -193,7 +208,7 @@ struct DmaTile {
   // Transfer i (of NI) of this wave for a tile whose rows are all valid.
   __device__ __forceinline__ void issue_one(const bf16_t *src, int i, bf16_t *lds) const {
     const int q = i * NW + wave;
-    if (kEven || q < T) dma_x4s(src, loff[i], lds_addr(lds) + q * 1024);
+    if (kEven || q < T) dma_x4s<NT>(src, loff[i], lds_addr(lds) + q * 1024);
   }
 
   // Rows [0, ROWS) of the tile starting at src (row stride rs elements); rows
@@ -205,7 +220,7 @@ struct DmaTile {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int q = i * NW + wave;
-        if (kEven || q < T) dma_x4s(src, loff[i], lb + q * 1024);
+        if (kEven || q < T) dma_x4s<NT>(src, loff[i], lb + q * 1024);
       }
     } else {
       // the lane index is re-read here (volatile, so not hoisted): a
@@ -219,7 +234,7 @@ struct DmaTile {
         if (!kEven && q >= T) continue;
         const int r = q * RPI + ln / CPR;
         const int rr = min(r, nvalid - 1);
-        dma_x4s(src, (uint32_t)(rr * rs + ((ln % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
+        dma_x4s<NT>(src, (uint32_t)(rr * rs + ((ln % CPR) ^ swz<D>(r)) * 8) * 2u, lb + q * 1024);
       }
     }
   }

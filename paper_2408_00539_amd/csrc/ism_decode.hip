@@ -9,8 +9,11 @@
 //    reads the new key/value from the input and also writes it into the
 //    cache, so no separate append launch is needed.
 //
-// Decode is a pure HBM stream (one query row per head: ~1 FLOP per byte), so
-// it uses VALU dot products, not MFMA.
+// Decode is an HBM stream (one query row per head: ~1 FLOP per byte per
+// head), so with 1-3 query heads per KV head it uses vector dot products;
+// with 4 or more the vector work would bound it, and a matrix-core kernel
+// takes those head sets (all heads of a KV head as the columns of one
+// product).
 #include "ism_common.h"
 #include "ism_kernels.h"
 
@@ -270,6 +273,188 @@ decode_split_kernel(DecodeArgs a) {
   }
 }
 
+// Decode step with matrix cores, for head sets of 4 or more query heads per
+// KV head (the vector kernel above is then bound by its FMAs, not by HBM).
+// One wave per workgroup streams one chunk of one (dialogue, KV head) slab
+// in 32-key tiles through a 2-stage LDS ring (direct global->LDS transfers,
+// the forward kernel's swizzled tile layout) and treats the set's query
+// heads as the 32 columns of the forward's products: S^T = K Q^T (lane <->
+// head, the columns past the set's heads hold zero queries and are never
+// written), an online softmax in exp2 form with the forward's lazy
+// rescaling, and O^T += V^T P^T with V^T through transposing reads. The
+// chunk holding the new position p patches the new key/value row into its
+// LDS tile (the cache row may not hold it yet: the first head set's owner
+// chunk writes it to the cache in the same launch). Chunks are whole tiles;
+// a tile of the paged cache lies inside one page (pages of 64k positions).
+// Partials (m in log2 units, l, o) go to the same split buffers as the
+// vector kernel's, merged by decode_combine_kernel.
+constexpr int kDecTile = 32;  // keys per tile
+template <int D>
+struct DecMmaSmem {
+  bf16_t k[2][kDecTile * D];
+  bf16_t v[2][kDecTile * D];
+};
+
+template <int D, bool PAGED>
+__global__ void __launch_bounds__(64)
+decode_mma_kernel(DecodeArgs a) {
+  constexpr int NKS = D / 16, NDB = D / 32, RB = 2 * D;
+  using Dma = DmaTile<D, kDecTile, 1, true>;  // the cache is read once per step
+  constexpr int NI = Dma::NI;  // transfers per tile and tensor
+  __shared__ DecMmaSmem<D> sm;
+
+  const int split = blockIdx.x, hs = blockIdx.y, b = blockIdx.z;
+  const int gs = a.set_heads, G = a.hq / a.hkv;
+  const int head0 = hs * gs, kvh = head0 / G;
+  const int lane = threadIdx.x, l32 = lane & 31, hf = lane >> 5;
+  // position of the new token, clamped as in the vector kernel
+  const int praw = __builtin_amdgcn_readfirstlane(a.pos[b]);
+  const bool in_cap = praw >= 0 && praw < a.cap;
+  const int p = min(max(praw, 0), a.cap - 1);
+  const int chunk = ((p + a.splits) / a.splits + kDecTile - 1) / kDecTile * kDecTile;
+  const int k0 = split * chunk, k1 = min(k0 + chunk, p + 1);
+  const int owner = p / chunk;
+  const float sl2 = a.scale * kLog2e;
+  const int64_t slab = ((int64_t)b * a.hkv + kvh) * a.cap * D;
+  auto row_of = [&](int t) -> int64_t {  // element offset of key t's row
+    if (PAGED)
+      return paged_offset_uniform(a.block_table, a.max_pages, a.num_pages, a.page_size, a.hkv,
+                                  D, b, kvh, t);
+    return slab + (int64_t)t * D;
+  };
+
+  // the new key/value row: 16 bytes per lane in lanes 0 .. D/8 - 1
+  constexpr int CPR = D / 8;
+  const bool patch = in_cap && split == owner;
+  u32x4 knew{}, vnew{};
+  if (patch && lane < CPR) {
+    const int64_t src = ((int64_t)b * a.hkv + kvh) * D + lane * 8;
+    knew = *(const u32x4 *)((const bf16_t *)a.k_new + src);
+    vnew = *(const u32x4 *)((const bf16_t *)a.v_new + src);
+    if (head0 % G == 0) {  // the KV head's first set stores it into the cache
+      const int64_t prow = row_of(p);
+      *(u32x4 *)((bf16_t *)a.k_cache + prow + lane * 8) = knew;
+      *(u32x4 *)((bf16_t *)a.v_cache + prow + lane * 8) = vnew;
+    }
+  }
+  // B operands of S^T = K Q^T: column l32 is query head head0 + l32
+  bf16x8 qf[NKS];
+  {
+    const bool real = l32 < gs;
+    const bf16_t *qp =
+        (const bf16_t *)a.q + ((int64_t)b * a.hq + head0 + (real ? l32 : 0)) * D + hf * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      qf[ks] = real ? *(const bf16x8 *)(qp + ks * 16) : bf16x8{};
+  }
+
+  Dma dma;
+  dma.init(lane, D);
+  SwzOffsets<D> so;
+  so.init(lane);
+  const int nt = k0 < k1 ? (k1 - k0 + kDecTile - 1) / kDecTile : 0;
+  auto issue = [&](int t) __attribute__((always_inline)) {  // tile t into stage t & 1
+    const int c = k0 + t * kDecTile;
+    const int64_t off = row_of(c);
+    const int nv = min(kDecTile, k1 - c);  // rows past it repeat the last valid one
+    dma.issue((const bf16_t *)a.k_cache + off, D, nv, sm.k[t & 1]);
+    dma.issue((const bf16_t *)a.v_cache + off, D, nv, sm.v[t & 1]);
+  };
+  wait_loads();  // queries, the new row and its store
+  if (nt > 0) issue(0);
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float tau = 8.f / sl2;  // lazy rescale threshold: 2^8 in probability units
+  for (int t = 0; t < nt; ++t) {
+    // tile t + 1 goes into the stage tile t - 1 used (its reads are done:
+    // their products consumed them); then wait for tile t only
+    if (t + 1 < nt) {
+      issue(t + 1);
+      wait_vmem_but<2 * NI>();
+    } else {
+      wait_vmem();
+    }
+    const int c0 = k0 + t * kDecTile;
+    bf16_t *kt = sm.k[t & 1];
+    bf16_t *vt = sm.v[t & 1];
+    if (patch && p - c0 < kDecTile && lane < CPR) {
+      const int r = p - c0;
+      const int e = r * D + ((lane ^ swz<D>(r)) << 3);
+      *(u32x4 *)(kt + e) = knew;
+      *(u32x4 *)(vt + e) = vnew;
+    }
+    const char *kl = (const char *)kt;
+    const char *vl = (const char *)vt;
+    f32x16 sc;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      sc = mfma32x32x16(*(const bf16x8 *)(kl + so.rowk[ks]), qf[ks], ks == 0 ? f32x16{} : sc);
+    if (c0 + kDecTile > k1) {  // the chunk's last tile: keys past k1 - 1 get -inf
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (c0 + (r >> 2) * 8 + hf * 4 + (r & 3) >= k1) sc[r] = -INFINITY;
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) mt = vmax(mt, vmax(sc[r], sc[r + 1]));
+    mt = pair_max(mt);
+    if (__builtin_amdgcn_ballot_w64(mt > m_run + tau) != 0) {
+      const float mnew = vmax(m_run, mt);
+      const float alpha = fast_exp2((m_run - mnew) * sl2);
+      m_run = mnew;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+    }
+    const float moff = m_run * sl2;
+    bf16x8 pf[2];
+    float sum = 0.f;
+#pragma unroll
+    for (int bt = 0; bt < 2; ++bt) {
+      u32x4 w;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        f32x2 pr;
+        pr[0] = fast_exp2(fmaf(sc[8 * bt + 2 * u], sl2, -moff));
+        pr[1] = fast_exp2(fmaf(sc[8 * bt + 2 * u + 1], sl2, -moff));
+        sum += pr[0] + pr[1];
+        w[u] = cvt_bf16x2(pr);
+      }
+      pf[bt] = __builtin_bit_cast(bf16x8, w);
+    }
+    l_run += sum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int bt = 0; bt < 2; ++bt) {
+        const uint32_t o = 16 * bt * RB;
+        oacc[db] = mfma32x32x16(tr_operand_at(vl, o + so.trk[db][0], o + so.trk[db][1]),
+                                pf[bt], oacc[db]);
+      }
+  }
+
+  // partials of the set's heads (an empty chunk: m = -inf, l = 0, o = 0)
+  const float lt = pair_sum(l_run);
+  if (l32 >= gs) return;
+  const int64_t pi = ((int64_t)b * a.hq + head0 + l32) * a.splits + split;
+  float *po = a.part_o + pi * D + hf * 4;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *(f32x4 *)(po + db * 32 + 8 * i) =
+          f32x4{oacc[db][4 * i], oacc[db][4 * i + 1], oacc[db][4 * i + 2], oacc[db][4 * i + 3]};
+  if (hf == 0) {
+    a.part_ml[pi * 2] = m_run * sl2;
+    a.part_ml[pi * 2 + 1] = lt;
+  }
+}
+
 // Exact merge of the split partials: M = max m_s, L = sum l_s 2^(m_s - M),
 // O = sum o_s 2^(m_s - M) / L. Scores were kept in log2 units. A dialogue
 // whose position lies outside the cache (out of contract) gets NaN.
@@ -319,8 +504,23 @@ hipError_t launch_decode_t(const DecodeArgs &a, hipStream_t stream) {
 }
 
 template <int D>
+hipError_t launch_decode_mma(const DecodeArgs &a, hipStream_t stream) {
+  const dim3 grid(a.splits, a.hq / a.set_heads, a.batch);
+  if (a.block_table)
+    hipLaunchKernelGGL((decode_mma_kernel<D, true>), grid, dim3(64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_mma_kernel<D, false>), grid, dim3(64), 0, stream, a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL((decode_combine_kernel<D>), dim3(a.batch * a.hq), dim3(D),
+                     0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
-  switch (decode_heads_per_set(a.hq, a.hkv)) {
+  if (a.mma) return launch_decode_mma<D>(a, stream);
+  switch (a.set_heads) {
     case 1: return launch_decode_t<D, 1>(a, stream);
     case 2: return launch_decode_t<D, 2>(a, stream);
     case 3: return launch_decode_t<D, 3>(a, stream);

@@ -109,13 +109,27 @@ struct DecodeArgs {
   // paged cache (see FwdArgs)
   const int32_t *block_table;
   int32_t page_size, max_pages, num_pages;
+  int32_t set_heads;  // query heads per workgroup (decode_heads_per_set)
+  int32_t mma;        // the matrix-core kernel (decode_mma_heads > 0)
 };
 
 hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream);
 
-// Query heads per decode workgroup: the largest divisor of G = hq / hkv
-// that is at most 8 (a workgroup keeps 8 + 10 registers per head).
+// Decode head sets, with G = hq / hkv query heads per KV head: the
+// matrix-core kernel takes sets of the largest divisor of G up to 32 (the
+// columns of one product) when that is 4 or more; 0 otherwise.
+inline int decode_mma_heads(int hq, int hkv) {
+  const int g = hq / hkv;
+  for (int s = g < 32 ? g : 32; s >= 4; --s)
+    if (g % s == 0) return s;
+  return 0;
+}
+// Query heads per decode workgroup: the matrix-core set, else (vector kernel)
+// the largest divisor of G that is at most 8 (it keeps 8 + 10 registers per
+// head).
 inline int decode_heads_per_set(int hq, int hkv) {
+  const int m = decode_mma_heads(hq, hkv);
+  if (m) return m;
   const int g = hq / hkv;
   for (int s = 8; s > 1; --s)
     if (g % s == 0) return s;
