@@ -97,17 +97,14 @@ __device__ __forceinline__ float group_sum(float x) {
 // G = hq / hkv and is at most 8, so that the per-head registers fit): head
 // set hs covers query heads hs GS .. hs GS + GS - 1 of KV head hs GS / G.
 // With G > 8 the G / GS sets of a KV head stream its keys separately.
-// Bounded to 256 registers, two waves per SIMD: only the paged variant for
-// sets of 8 heads needs the bound (unbounded it took 262 registers and ran
-// one wave per SIMD; bounded, with 6 registers spilled, a step over 32
-// dialogues at position 8192 with 8 query heads per KV head takes 0.315
-// instead of 0.414 ms).
+// Sets of 4 or more heads go to decode_mma_kernel below, so GS <= 3 here.
 template <int D, int GS, bool PAGED>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
+  static_assert(GS >= 1 && GS <= 3, "larger head sets run on the matrix cores");
   constexpr int CPK = D / 8;     // lanes per key row (16 bytes each)
   constexpr int KPI = 64 / CPK;  // keys per wave-wide load
-  constexpr int U = GS > 4 ? 4 : 8;  // loads in flight per lane per tensor
+  constexpr int U = 8;           // loads in flight per lane per tensor
   constexpr int KPW = U * KPI;   // keys per wave per iteration
   __shared__ float sm_o[4][GS][D];
   __shared__ float sm_m[4][GS], sm_l[4][GS];
@@ -524,11 +521,6 @@ hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
     case 1: return launch_decode_t<D, 1>(a, stream);
     case 2: return launch_decode_t<D, 2>(a, stream);
     case 3: return launch_decode_t<D, 3>(a, stream);
-    case 4: return launch_decode_t<D, 4>(a, stream);
-    case 5: return launch_decode_t<D, 5>(a, stream);
-    case 6: return launch_decode_t<D, 6>(a, stream);
-    case 7: return launch_decode_t<D, 7>(a, stream);
-    case 8: return launch_decode_t<D, 8>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }

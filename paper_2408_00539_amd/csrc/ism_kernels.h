@@ -124,16 +124,13 @@ inline int decode_mma_heads(int hq, int hkv) {
     if (g % s == 0) return s;
   return 0;
 }
-// Query heads per decode workgroup: the matrix-core set, else (vector kernel)
-// the largest divisor of G that is at most 8 (it keeps 8 + 10 registers per
-// head).
+// Query heads per decode workgroup: the matrix-core set, else (vector kernel,
+// G without a divisor between 4 and 32) the largest divisor of G up to 3.
 inline int decode_heads_per_set(int hq, int hkv) {
   const int m = decode_mma_heads(hq, hkv);
   if (m) return m;
   const int g = hq / hkv;
-  for (int s = 8; s > 1; --s)
-    if (g % s == 0) return s;
-  return 1;
+  return g % 3 == 0 ? 3 : g % 2 == 0 ? 2 : 1;
 }
 
 struct BwdArgs {
