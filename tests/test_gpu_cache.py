@@ -35,7 +35,8 @@ def _setup(rng, hist, new, hq, hkv, d, cap):
 
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (8, 2), (4, 1), (8, 1),
-                                    (3, 1), (12, 1), (16, 2), (6, 3)])
+                                    (3, 1), (12, 1), (16, 2), (6, 3), (5, 1), (32, 1),
+                                    (64, 1)])
 def test_prefill_then_decode_small(d, hq, hkv):
     torch = torch_cuda()
     from paper_2408_00539_amd import ops
@@ -125,12 +126,15 @@ def test_prefill_answer_segment_small(d, hq, hkv):
             compare(f"LSE b{b} q={isq}", lse[:, r0:r1], rl)
 
 
-def test_decode_split_counts_agree():
-    """Any split count merges to the same result (exact merge, R19)."""
+@pytest.mark.parametrize("hq,hkv", [(4, 4), (16, 2)])
+def test_decode_split_counts_agree(hq, hkv):
+    """Any split count merges to the same result (exact merge, R19), for the
+    vector kernel (one query head per KV head) and the matrix-core kernel
+    (8); with 64 splits most chunks of the shorter dialogues are empty."""
     torch = torch_cuda()
     from paper_2408_00539_amd import ops
     rng = np.random.default_rng(77)
-    B, hq, hkv, d, cap = 3, 4, 4, 128, 2048
+    B, d, cap = 3, 128, 2048
     kc = _bits(rng, B, hkv, cap, d)
     vc = _bits(rng, B, hkv, cap, d)
     pos = np.array([0, 1000, 2047], np.int32)
