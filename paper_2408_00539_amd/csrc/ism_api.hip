@@ -90,17 +90,18 @@ ism_status hip_status(hipError_t e, const char *what) {
   return fail(ISM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Split count of a decode step; `sets` = head sets per dialogue (hkv when
-// hq / hkv <= 8).
-int decode_splits(int32_t batch, int32_t sets, int32_t max_len, int32_t req, bool mma) {
+// Split count of a decode step; `sets` = head sets per dialogue
+// (hq / decode_heads_per_set), `target` = workgroups to aim at: about 2048
+// four-wave workgroups (two rounds of four per CU) for the vector kernel;
+// for the matrix-core kernel, whose long chunks stream faster, about 512
+// one-wave workgroups on a dense cache and 768 on a paged one (on 256 slabs
+// of 8192 keys: 6.5 and 6.4 TB/s, against 6.2 and 6.4 with 768 for both,
+// 6.5 and 6.0 with 512, and 5.5 and 5.5 with 4096). At least 256 keys per
+// chunk, at most 64 chunks.
+constexpr int kSplitsVector = 2048, kSplitsMmaDense = 512, kSplitsMmaPaged = 768;
+int decode_splits(int32_t batch, int32_t sets, int32_t max_len, int32_t req, int target) {
   if (req > 0) return req;
-  // about 2048 four-wave workgroups (two rounds of four per CU) for the
-  // vector kernel; about 768 one-wave workgroups (three per CU) for the
-  // matrix-core kernel, whose long chunks stream faster (on 256 slabs of 8192
-  // keys: 6.2 TB/s dense and 6.4 paged, against 5.5 and 5.5 with 4096 and
-  // 6.1 and 6.3 with 1024); at least 256 keys per chunk, at most 64 chunks
   const int slabs = batch * sets;
-  const int target = mma ? 768 : 2048;
   int s = (target + slabs - 1) / slabs;
   const int by_len = (max_len + 255) / 256;
   if (s > by_len) s = by_len;
@@ -125,9 +126,11 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
       return 0;
     case ISM_OP_DECODE: {
       if (hkv < 1 || hq < hkv || hq % hkv) return 0;
+      // the larger of the dense and paged split counts
       const int sets = hq / ism::decode_heads_per_set(hq, hkv);
-      const size_t s = (size_t)decode_splits(batch, sets, max_seqlen, num_splits,
-                                             ism::decode_mma_heads(hq, hkv) > 0);
+      const size_t s = (size_t)decode_splits(
+          batch, sets, max_seqlen, num_splits,
+          ism::decode_mma_heads(hq, hkv) > 0 ? kSplitsMmaPaged : kSplitsVector);
       return align_up((size_t)batch * hq * s * d * 4) +
              align_up((size_t)batch * hq * s * 2 * 4);
     }
@@ -438,7 +441,8 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
     return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
   const int set_heads = ism::decode_heads_per_set(hq, hkv);
   const bool mma = ism::decode_mma_heads(hq, hkv) > 0;
-  const int splits = decode_splits(batch, hq / set_heads, max_seqlen, num_splits, mma);
+  const int splits = decode_splits(batch, hq / set_heads, max_seqlen, num_splits,
+                                   !mma ? kSplitsVector : pg ? kSplitsMmaPaged : kSplitsMmaDense);
   const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen, hq,
                                               hkv, d, num_splits);
   if ((st = check_ws(ws, ws_bytes, need))) return st;

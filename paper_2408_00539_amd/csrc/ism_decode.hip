@@ -281,8 +281,9 @@ decode_split_kernel(DecodeArgs a) {
 // rescaling, and O^T += V^T P^T with V^T through transposing reads. The
 // chunk holding the new position p patches the new key/value row into its
 // LDS tile (the cache row may not hold it yet: the first head set's owner
-// chunk writes it to the cache in the same launch). Chunks are whole tiles;
-// a tile of the paged cache lies inside one page (pages of 64k positions).
+// chunk writes it to the cache in the same launch). Chunks are whole tiles,
+// so a tile of the paged cache lies inside one page (page sizes are
+// multiples of 64 positions).
 // Partials (m in log2 units, l, o) go to the same split buffers as the
 // vector kernel's, merged by decode_combine_kernel.
 constexpr int kDecTile = 32;  // keys per tile

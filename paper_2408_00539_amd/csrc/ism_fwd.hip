@@ -446,7 +446,8 @@ fwd_kernel(FwdArgs a, int hpw, int tiles, int chunk) {
     };
     if (t < nw) {
       float mt;
-      l_run += step_block<D, LAST, !PAGED>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt, hook);
+      l_run += step_block<D, LAST, !PAGED>(kl, vl, so, qf, cur, nxt, oacc, sl2, m_run * sl2, mt,
+                                           hook);
       if (!LAST && t + 1 < nw) {
         if (c0 + 2 * kBN - 1 > wave_lo) {  // S(t+1) crosses some row's bound
           tile_mask(nxt, c0 + kBN, hf, lim_r);
