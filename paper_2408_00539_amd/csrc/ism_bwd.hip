@@ -75,9 +75,13 @@ constexpr int kDkvStages = 3;
 
 // Q and dO tiles of 64 rows (unpadded swizzled rows, see swz<D>()) plus the
 // per-row -lse / scale and -delta as two planes of bf16 summands, all filled
-// by direct global->LDS transfers; and P of the last two tiles for each wave pair in the bf16 B
-// operand form of the dV product (lane-private, 4 x 16 bytes per lane, laid
-// out so that consecutive lanes touch consecutive bytes).
+// by direct global->LDS transfers; and P of the last two tiles for each
+// wave pair as fp16 pairs in the element order of the dV product's bf16 B
+// operand (lane-private, 4 x 16 bytes per lane, laid out so that
+// consecutive lanes touch consecutive bytes). fp16 rather than bf16: P lies
+// in [0, 1], where fp16 keeps 3 more mantissa bits, so the dS wave's
+// dS = P o (dP - delta) carries one rounding of P 8x smaller than bf16's,
+// and its fp16 x fp32 products are single v_fma_mix_f32 instructions.
 template <int D>
 struct DkvSmem {
   bf16_t q[kDkvStages][kBR * D];
@@ -118,7 +122,7 @@ __device__ __forceinline__ void product_stream(Rd &&rd, Mm &&mm, Mid &&mid) {
 // Eight waves in four pairs; pair p owns the 32 keys c0 + 32 p (lane <->
 // key) and its two waves share one SIMD. Per 64-row tile t:
 //  * the P wave (p) computes S = Q K^T and P = exp(S - LSE) (masked),
-//    accumulates dV^T += dO^T P and leaves P (bf16) in LDS;
+//    accumulates dV^T += dO^T P (P in bf16) and leaves P (fp16) in LDS;
 //  * the dS wave (p + 4), one tile behind, forms dS = P o (dP - delta) with
 //    its partner's P and accumulates dK^T += Q^T dS, then computes
 //    dP = dO V^T of tile t for the next step.
@@ -249,8 +253,8 @@ dkv_kernel(BwdArgs a, int ktiles) {
     auto ds_pair = [&](int kk, int u) __attribute__((always_inline)) {
       const int rb = kk >> 1, e0 = 8 * (kk & 1) + 2 * u;
       f32x2 x;
-      x[0] = bf16_lo(pw[kk][u]) * dp[rb][e0];
-      x[1] = bf16_hi(pw[kk][u]) * dp[rb][e0 + 1];
+      x[0] = mul_f16_lo(pw[kk][u], dp[rb][e0]);
+      x[1] = mul_f16_hi(pw[kk][u], dp[rb][e0 + 1]);
       uint32_t w = cvt_bf16x2(x);
       asm volatile("" : "+v"(w));
       fw[kk][u] = w;
@@ -306,15 +310,15 @@ dkv_kernel(BwdArgs a, int ktiles) {
   // at the row's -lse / scale (so that P = exp2(acc * scale * log2 e)), S
   // of row block 0, S of row block 1 beside the exponentials of block 0,
   // dV^T += dO^T P for block 0 beside the exponentials of block 1, then dV
-  // for block 1. P goes to LDS (and into
-  // operand form) in 16-row slices; rows are masked unless every row sees
-  // every key.
+  // for block 1. P goes to LDS as fp16 (and into bf16 operand form) in
+  // 16-row slices; rows are masked unless every row sees every key.
   auto p_dv = [&](int st, int r0, int nvalid, bool full) __attribute__((always_inline)) {
     const char *ql = (const char *)sm.q[st];
     const char *dl = (const char *)sm.dout[st];
     u32x4 *pp = sm.p[st][pair];
     f32x16 sacc[NRB];
     u32x4 fw[NKK];
+    u32x4 hw;  // the slice being formed, as fp16 pairs for the dS wave
     constexpr int NX = NRB;        // summand products, then
     constexpr int NS = NKS * NRB;  // S products, row-block major
     constexpr int EPS = 16 / NKS;  // exponentials per slot
@@ -370,10 +374,11 @@ dkv_kernel(BwdArgs a, int ktiles) {
           f32x2 x;
           x[0] = fast_exp2(sacc[rb][e0] * sl2);
           x[1] = fast_exp2(sacc[rb][e0 + 1] * sl2);
-          uint32_t p2 = cvt_bf16x2(x);
-          asm volatile("" : "+v"(p2));
+          uint32_t p2 = cvt_bf16x2(x), h2 = cvt_f16x2(x);
+          asm volatile("" : "+v"(p2), "+v"(h2));
           fw[2 * rb + (e0 >> 3)][(e0 & 7) >> 1] = p2;
-          if ((e0 & 7) == 6) pp[(2 * rb + (e0 >> 3)) * 64 + lane] = fw[2 * rb + (e0 >> 3)];
+          hw[(e0 & 7) >> 1] = h2;
+          if ((e0 & 7) == 6) pp[(2 * rb + (e0 >> 3)) * 64 + lane] = hw;
         }
       }
     };

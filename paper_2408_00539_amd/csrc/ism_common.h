@@ -72,6 +72,22 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return cvt_bf16x2(f32x2{lo, hi});
 }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed fp16 pair in one v_cvt_pk_f16_f32 (round to nearest even).
+__device__ __forceinline__ uint32_t cvt_f16x2(f32x2 v) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));
+}
+
+// The low / high fp16 half of w times an fp32 value, as one v_fma_mix_f32
+// (the conversion is exact, the product rounds once).
+__device__ __forceinline__ float mul_f16_lo(uint32_t w, float b) {
+  return __builtin_fmaf((float)__builtin_bit_cast(f16x2, w).x, b, 0.f);
+}
+__device__ __forceinline__ float mul_f16_hi(uint32_t w, float b) {
+  return __builtin_fmaf((float)__builtin_bit_cast(f16x2, w).y, b, 0.f);
+}
+
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // A operand (32 x 16, bf16) of a 32x32x16 MFMA read from a tile stored with

@@ -1,9 +1,11 @@
 """GPU parity on generated layouts: hypothesis draws packed batches of
 dialogues whose segment lengths sit on and around the kernels' tile sizes
 (1, 31-33, 63-65, 127-129 and others), with arbitrary query/answer flag
-patterns (Eq. 5 for every pattern, R2), head groupings of 1, 2, 4 and 8 and
-both head dims, and compares the forward and the backward with the fp64
-oracle. Derandomized: the same examples run every time."""
+patterns (Eq. 5 for every pattern, R2), head groupings of 1, 2, 3, 4 and 8
+and both head dims, and compares the forward and the backward with the fp64
+oracle; the cache-path tests add groupings of 5, 6, 12 and 16 query heads
+per KV head (the decode's matrix-core sets). Derandomized: the same examples
+run every time."""
 
 import numpy as np
 import pytest
@@ -20,7 +22,10 @@ pytestmark = pytest.mark.gpu
 EDGE = [1, 2, 31, 32, 33, 63, 64, 65, 127, 128, 129]
 seg_len = st.one_of(st.sampled_from(EDGE), st.integers(1, 200))
 dialogue = st.lists(st.tuples(seg_len, st.booleans()), min_size=1, max_size=6)
-heads = st.sampled_from([(1, 1), (2, 1), (2, 2), (4, 1), (4, 2), (8, 1), (8, 2), (8, 8)])
+heads = st.sampled_from([(1, 1), (2, 1), (2, 2), (4, 1), (4, 2), (8, 1), (8, 2), (8, 8),
+                         (3, 1), (6, 2)])
+cache_heads = st.sampled_from([(1, 1), (2, 1), (2, 2), (4, 1), (4, 2), (8, 1), (8, 2), (8, 8),
+                               (3, 1), (5, 1), (6, 1), (12, 2), (16, 1)])
 
 
 @settings(max_examples=60, deadline=None, derandomize=True, database=None)
@@ -61,7 +66,7 @@ new_len = st.one_of(st.sampled_from([1, 2, 31, 32, 33, 63, 64, 65]), st.integers
 
 @settings(max_examples=40, deadline=None, derandomize=True, database=None)
 @given(turns=st.lists(st.tuples(hist_len, new_len), min_size=1, max_size=4),
-       is_query=st.booleans(), hh=heads, d=st.sampled_from([64, 128]),
+       is_query=st.booleans(), hh=cache_heads, d=st.sampled_from([64, 128]),
        splits=st.sampled_from([0, 1, 3, 64]), seed=st.integers(0, 2 ** 31 - 1))
 def test_generated_cache_turns(turns, is_query, hh, d, splits, seed):
     """Cached prefill of a query or answer segment over generated histories,
@@ -119,7 +124,7 @@ def test_generated_cache_turns(turns, is_query, hh, d, splits, seed):
 
 @settings(max_examples=30, deadline=None, derandomize=True, database=None)
 @given(turns=st.lists(st.tuples(hist_len, new_len), min_size=1, max_size=4),
-       is_query=st.booleans(), hh=heads, d=st.sampled_from([64, 128]),
+       is_query=st.booleans(), hh=cache_heads, d=st.sampled_from([64, 128]),
        page_size=st.sampled_from([64, 128, 192, 256]), splits=st.sampled_from([0, 2, 7]),
        seed=st.integers(0, 2 ** 31 - 1))
 def test_generated_paged_equals_dense(turns, is_query, hh, d, page_size, splits, seed):
