@@ -175,7 +175,9 @@ ism_status ism_attn_prefill_cached_segment(
  * host, where the positions (device memory) are not. Workspace:
  * ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen (with 0
  * replaced by cache_cap), hq, hkv, d, num_splits). Any hq / hkv is
- * supported; a workgroup serves up to 8 query heads of one KV head. */
+ * supported: with 4 or more query heads per KV head a workgroup serves a
+ * set of 4-32 of them on the matrix cores, otherwise 1-3 on the vector
+ * ALU. */
 ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            void *k_cache, void *v_cache, int32_t cache_cap,
                            const int32_t *cache_seqlens, int32_t batch,
