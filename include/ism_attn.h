@@ -23,7 +23,8 @@
  *    and d = 128.
  *  - `scale` multiplies Q K^T before the softmax (normally 1/sqrt(d)).
  *  - All work is enqueued on `stream` (a hipStream_t passed as void*, NULL =
- *    the default stream). No call synchronises the device.
+ *    the default stream). No call synchronises the device (except under
+ *    ISM_VALIDATE=1, below).
  *  - `ws` is a caller-owned device workspace of at least
  *    ism_attn_workspace_size(...) bytes, 256-byte aligned.
  *  - On any error no kernel is launched, outputs are untouched, and a status
@@ -32,7 +33,13 @@
  *    synchronisation of the stream, as for any HIP kernel.
  *  - Device-resident segment arrays are not inspected by the entry points
  *    (that would need a synchronising copy); ism_check_segments_host()
- *    validates a host copy of them.
+ *    validates a host copy of them. For debugging, the environment variable
+ *    ISM_VALIDATE=1 (read on every call) makes each entry point that takes
+ *    an ism_segments, and each cached prefill (cu_seqlens_new: from 0 to
+ *    total_new, non-decreasing, no length above max_new), wait for its
+ *    stream, copy those arrays to the host and validate them before any
+ *    launch, failing with the validator's status (ISM_ERR_SEGMENTS for
+ *    malformed boundaries).
  *  - No entry point aborts, throws or exits the process.
  */
 #ifndef ISM_ATTN_H

@@ -1,10 +1,13 @@
 // C ABI of the ISM attention library: argument checks, workspace layout and
 // the launch sequence of each entry point. Every check happens on the host
-// before any launch; nothing here synchronises the device.
+// before any launch; nothing here synchronises the device, except the
+// optional segment validation below (ISM_VALIDATE=1).
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
+#include <vector>
 
 #include "../../include/ism_attn.h"
 #include "ism_host.h"
@@ -90,6 +93,49 @@ ism_status hip_status(hipError_t e, const char *what) {
   return fail(ISM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Optional validation of the device segment arrays, for debugging: with the
+// environment variable ISM_VALIDATE set to 1 (read on every call), an entry
+// point that takes an ism_segments waits for its stream, copies the three
+// arrays to the host and runs ism_check_segments_host before any launch,
+// so malformed metadata fails with its status instead of reaching the
+// kernels. A device round trip per call; off by default.
+ism_status validate_segments(const ism_segments *sg, hipStream_t stream) {
+  const char *v = getenv("ISM_VALIDATE");
+  if (!v || strcmp(v, "1") != 0) return ISM_OK;
+  std::vector<int32_t> cu(sg->batch + 1), cs(sg->num_segs + 1);
+  std::vector<uint8_t> fl(sg->num_segs);
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e == hipSuccess)
+    e = hipMemcpy(cu.data(), sg->cu_seqlens, cu.size() * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess)
+    e = hipMemcpy(cs.data(), sg->cu_segs, cs.size() * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(fl.data(), sg->seg_is_query, fl.size(), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_status(e, "ISM_VALIDATE: copying the segment arrays");
+  return ism_check_segments_host(cu.data(), cs.data(), fl.data(), sg->batch, sg->num_segs,
+                                 sg->total_tokens, sg->max_seqlen);
+}
+
+// The same for the new-token boundaries of a cached prefill: cu_seqlens_new
+// starts at 0, ends at total_new and never decreases, and no dialogue has
+// more than max_new new tokens.
+ism_status validate_new_lengths(const int32_t *cu_new, int32_t batch, int32_t total_new,
+                                int32_t max_new, hipStream_t stream) {
+  const char *v = getenv("ISM_VALIDATE");
+  if (!v || strcmp(v, "1") != 0) return ISM_OK;
+  std::vector<int32_t> cu(batch + 1);
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e == hipSuccess) e = hipMemcpy(cu.data(), cu_new, cu.size() * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_status(e, "ISM_VALIDATE: copying cu_seqlens_new");
+  if (cu[0] != 0 || cu[batch] != total_new)
+    return fail(ISM_ERR_SEGMENTS, "cu_seqlens_new must run from 0 to total_new=%d (got %d..%d)",
+                total_new, cu[0], cu[batch]);
+  for (int32_t b = 0; b < batch; ++b)
+    if (cu[b + 1] < cu[b] || cu[b + 1] - cu[b] > max_new)
+      return fail(ISM_ERR_SEGMENTS, "dialogue %d has %d new tokens (need 0..max_new=%d)", b,
+                  cu[b + 1] - cu[b], max_new);
+  return ISM_OK;
+}
+
 // Split count of a decode step; `sets` = head sets per dialogue
 // (hq / decode_heads_per_set), `target` = workgroups to aim at: about 2048
 // four-wave workgroups (two rounds of four per CU) for the vector kernel;
@@ -152,6 +198,7 @@ extern "C" ism_status ism_attn_fwd(const ism_segments *sg, const void *q,
                                               sg->max_seqlen, hq, hkv, d, 0);
   if ((st = check_ws(ws, ws_bytes, need))) return st;
   if ((st = check_device())) return st;
+  if ((st = validate_segments(sg, (hipStream_t)stream))) return st;
 
   hipStream_t s = (hipStream_t)stream;
   int32_t *lim = (int32_t *)ws;
@@ -181,6 +228,7 @@ extern "C" ism_status ism_visibility(const ism_segments *sg, int32_t *lim, int32
   if (st) return st;
   if (!lim || !seer) return fail(ISM_ERR_NULL, "lim and seer are required");
   if ((st = check_device())) return st;
+  if ((st = validate_segments(sg, (hipStream_t)stream))) return st;
   return hip_status(ism::launch_bwd_prep(sg->cu_segs, sg->seg_is_query, sg->num_segs,
                                          sg->total_tokens, lim, seer, (hipStream_t)stream),
                     "visibility launch");
@@ -202,6 +250,7 @@ extern "C" ism_status ism_attn_bwd(const ism_segments *sg, const void *q,
                                               sg->max_seqlen, hq, hkv, d, 0);
   if ((st = check_ws(ws, ws_bytes, need))) return st;
   if ((st = check_device())) return st;
+  if ((st = validate_segments(sg, (hipStream_t)stream))) return st;
 
   hipStream_t s = (hipStream_t)stream;
   const size_t tb = align_up((size_t)sg->total_tokens * 4);
@@ -303,6 +352,9 @@ ism_status prefill_impl(const int32_t *cu_seqlens_new, int32_t batch, int32_t to
   }
   (void)ws; (void)ws_bytes;
   if ((st = check_device())) return st;
+  if ((st = validate_new_lengths(cu_seqlens_new, batch, total_new, max_new,
+                                 (hipStream_t)stream)))
+    return st;
 
   hipStream_t s = (hipStream_t)stream;
   const float l2b = rp ? log2f(rp->base) : 0.f;
@@ -376,6 +428,7 @@ extern "C" ism_status ism_positions_2d(const ism_segments *sg, int32_t *pos1, in
   if (st) return st;
   if (!pos1 || !pos2) return fail(ISM_ERR_NULL, "pos1 and pos2 are required");
   if ((st = check_device())) return st;
+  if ((st = validate_segments(sg, (hipStream_t)stream))) return st;
   return hip_status(ism::launch_positions_2d(sg->cu_seqlens, sg->batch, sg->cu_segs,
                                              sg->num_segs, sg->total_tokens, pos1, pos2,
                                              (hipStream_t)stream),
