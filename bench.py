@@ -154,8 +154,21 @@ def device_info():
                 info["compute_units"] = int(val)
             elif key == "Max Clock Freq. (MHz)" and "max_clock_mhz" not in info:
                 info["max_clock_mhz"] = int(val)
+        info.update(_versions())
         return info
     return None
+
+
+def _versions():
+    """ROCm (the installed release), HIP and torch versions."""
+    import torch
+    v = {"torch": torch.__version__, "hip": torch.version.hip}
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            v["rocm"] = f.read().strip()
+    except OSError:
+        pass
+    return v
 
 
 def bench_training(w, timer, steps, warmup, with_bwd):
@@ -505,7 +518,7 @@ def _f64(bits):
     return bf16_bits_to_f32(bits).astype(np.float64)
 
 
-def cpu_baseline(w4, w1=None, w2=None, w3=None):
+def cpu_baseline(w4, w1=None, w2=None, w3=None, gpu4=None):
     """The fp64 oracle (test infrastructure, as it stands) on bounded samples
     of the workloads, on the host cores; one (dialogue, head) pair per
     thread, one BLAS thread each.
@@ -516,7 +529,13 @@ def cpu_baseline(w4, w1=None, w2=None, w3=None):
     (`workers` pairs), and workload 3's cache path for one dialogue (the
     one-shot reference rows of its new query segment and 16 answer tokens,
     then the same 16 tokens as stepwise decode steps after the cached
-    prefill, as the per-step time and its K/V bytes per second)."""
+    prefill, as the per-step time and its K/V bytes per second).
+
+    gpu4 = (o, lse, dq, dk, dv), the device outputs of one step of workload
+    4: after the timing, the headline sample's oracle results are compared
+    with them on its pairs (max / mean absolute error per tensor, the
+    parity bar's two terms), so the line carries the parity of what it
+    timed."""
     import oracle
     from threadpoolctl import threadpool_limits
     cores = len(os.sched_getaffinity(0))
@@ -532,10 +551,12 @@ def cpu_baseline(w4, w1=None, w2=None, w3=None):
         args = (w4.segs.cu_seqlens, w4.segs.cu_segs, w4.segs.seg_is_query, w4.scale)
         pairs = [(b, h) for b in range(w4.segs.batch) for h in range(w4.hq)][:workers]
         t0 = time.perf_counter()
-        oracle.fwd(q, k, v, *args, pairs=pairs, workers=workers)
-        oracle.bwd(q, k, v, do, *args, pairs=pairs, workers=workers)
+        ref = oracle.fwd(q, k, v, *args, pairs=pairs, workers=workers)
+        ref += oracle.bwd(q, k, v, do, *args, pairs=pairs, workers=workers)
         dt = time.perf_counter() - t0
         flop = pairs_flop(w4, pairs, 14)
+        if gpu4 is not None:
+            out["parity"] = _sample_parity(w4, pairs, gpu4, ref)
         out.update({"value": flop / dt / 1e12, "seconds": round(dt, 2),
                     "sample": f"fp64 oracle forward + backward of workload 4 (4 x 8192, "
                               f"32 heads, d 128) on {len(pairs)} of "
@@ -562,6 +583,28 @@ def cpu_baseline(w4, w1=None, w2=None, w3=None):
         if w3 is not None:
             out["legs"]["cache_32x8192"] = _cpu_cache_leg(oracle, w3, workers)
     return out
+
+
+def _sample_parity(w, pairs, gpu, ref):
+    """Max and mean absolute error of the device outputs against the
+    oracle's on the (dialogue, head) pairs it computed."""
+    names = ("O", "LSE", "dQ", "dK", "dV")
+    cu = w.segs.cu_seqlens
+    G = w.hq // w.hkv
+    res = {"pairs": len(pairs)}
+    for name, g, r in zip(names, gpu, ref):
+        errs = []
+        for b, h in pairs:
+            s, e = int(cu[b]), int(cu[b + 1])
+            hh = h // G if name in ("dK", "dV") else h
+            if name == "LSE":
+                gv, rv = g[hh, s:e], r[hh, s:e]
+            else:
+                gv, rv = g[s:e, hh], r[s:e, hh]
+            errs.append(np.abs(gv.float().cpu().numpy().astype(np.float64) - rv).ravel())
+        err = np.concatenate(errs)
+        res[name] = {"max_abs": float(err.max()), "mean_abs": float(err.mean())}
+    return res
 
 
 def _cpu_cache_leg(oracle, w, workers, steps=16):
@@ -863,8 +906,15 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
+        # one more step of workload 4, its outputs for the parity report
+        segs4 = ops.Segments.from_host(w4.segs.cu_seqlens, w4.segs.cu_segs,
+                                       w4.segs.seg_is_query)
+        q4, k4, v4, do4 = dev(w4.q), dev(w4.k), dev(w4.v), dev(w4.do)
+        o4, l4 = ops.fwd(q4, k4, v4, segs4, w4.scale)
+        gpu4 = (o4, l4) + tuple(ops.bwd(q4, k4, v4, o4, l4, do4, segs4, w4.scale))
+        torch.cuda.synchronize()
         log("timing the CPU oracle ...")
-        cpu = cpu_baseline(w4, w1, w2, w3)
+        cpu = cpu_baseline(w4, w1, w2, w3, gpu4)
 
     value = step_flop / step_ms / 1e9
     line = {
