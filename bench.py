@@ -541,7 +541,7 @@ def cpu_baseline(w4, w1=None, w2=None, w3=None, gpu4=None):
     cores = len(os.sched_getaffinity(0))
     workers = max(1, min(cores, 16))
     out = {"unit": "TFLOP/s", "cores": workers, "kind": "oracle",
-           "cpu": _cpu_model(), "legs": {}}
+           "cpu": _cpu_model(), "blas": _blas_name(), "legs": {}}
 
     def pairs_flop(w, pairs, per_pair):
         return per_pair * w.d * sum(_pairs_of_dialogue(w.segs, b) for b, _ in pairs)
@@ -564,7 +564,10 @@ def cpu_baseline(w4, w1=None, w2=None, w3=None, gpu4=None):
                               f"{workers} threads, {dt:.1f} s wall; useful FLOPs "
                               f"of those pairs (14 d per visible pair)"})
         del q, k, v, do
-        for name, w, full in (("fwd_8x4096", w1, True), ("fwd_gqa_2x16384", w2, False)):
+        from paper_2408_00539_amd import workloads as W
+        w0 = W.make_workload(0)
+        for name, w, full in (("fwd_small", w0, True), ("fwd_8x4096", w1, True),
+                              ("fwd_gqa_2x16384", w2, False)):
             if w is None:
                 continue
             q, k, v = _f64(w.q), _f64(w.k), _f64(w.v)
@@ -660,6 +663,14 @@ def _pairs_of_dialogue(segs, b):
     return visible_pairs(SimpleNamespace(
         cu_seqlens=np.array([0, e - s]), cu_segs=cs[g0:g1 + 1] - s,
         seg_is_query=np.asarray(segs.seg_is_query)[g0:g1]))
+
+
+def _blas_name():
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        return f"{b.get('name')} {b.get('version')}"
+    except Exception:  # older numpy: no dict form
+        return None
 
 
 def _cpu_model():
