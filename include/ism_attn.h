@@ -184,7 +184,8 @@ ism_status ism_attn_prefill_cached_segment(
  * replaced by cache_cap), hq, hkv, d, num_splits). Any hq / hkv is
  * supported: with 4 or more query heads per KV head a workgroup serves a
  * set of 4-32 of them on the matrix cores, otherwise 1-3 on the vector
- * ALU. */
+ * ALU, except that a step with fewer than 512 (dialogue, KV head) pairs
+ * runs every head set on the matrix cores. */
 ism_status ism_attn_decode(const void *q, const void *k_new, const void *v_new,
                            void *k_cache, void *v_cache, int32_t cache_cap,
                            const int32_t *cache_seqlens, int32_t batch,

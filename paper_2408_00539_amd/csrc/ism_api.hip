@@ -173,10 +173,10 @@ extern "C" size_t ism_attn_workspace_size(int32_t op, int32_t batch,
     case ISM_OP_DECODE: {
       if (hkv < 1 || hq < hkv || hq % hkv) return 0;
       // the larger of the dense and paged split counts
-      const int sets = hq / ism::decode_heads_per_set(hq, hkv);
+      const int sets = hq / ism::decode_heads_per_set(batch, hq, hkv);
       const size_t s = (size_t)decode_splits(
           batch, sets, max_seqlen, num_splits,
-          ism::decode_mma_heads(hq, hkv) > 0 ? kSplitsMmaPaged : kSplitsVector);
+          ism::decode_mma_heads(batch, hq, hkv) > 0 ? kSplitsMmaPaged : kSplitsVector);
       return align_up((size_t)batch * hq * s * d * 4) +
              align_up((size_t)batch * hq * s * 2 * 4);
     }
@@ -492,8 +492,8 @@ ism_status decode_impl(const void *q, const void *k_new, const void *v_new, void
                 cache_cap);
   if (num_splits < 0 || num_splits > 1024)
     return fail(ISM_ERR_SHAPE, "num_splits %d outside [0, 1024]", num_splits);
-  const int set_heads = ism::decode_heads_per_set(hq, hkv);
-  const bool mma = ism::decode_mma_heads(hq, hkv) > 0;
+  const int set_heads = ism::decode_heads_per_set(batch, hq, hkv);
+  const bool mma = ism::decode_mma_heads(batch, hq, hkv) > 0;
   const int splits = decode_splits(batch, hq / set_heads, max_seqlen, num_splits,
                                    !mma ? kSplitsVector : pg ? kSplitsMmaPaged : kSplitsMmaDense);
   const size_t need = ism_attn_workspace_size(ISM_OP_DECODE, batch, 0, max_seqlen, hq,

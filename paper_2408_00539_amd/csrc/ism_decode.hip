@@ -10,10 +10,12 @@
 //    cache, so no separate append launch is needed.
 //
 // Decode is an HBM stream (one query row per head: ~1 FLOP per byte per
-// head), so with 1-3 query heads per KV head it uses vector dot products;
-// with 4 or more the vector work would bound it, and a matrix-core kernel
-// takes those head sets (all heads of a KV head as the columns of one
-// product).
+// head), so with 1-3 query heads per KV head it can use vector dot
+// products; with 4 or more the vector work would bound it, and a
+// matrix-core kernel takes those head sets (all heads of a KV head as the
+// columns of one product). The matrix-core kernel also takes 1-3 heads when
+// the step has few (dialogue, KV head) slabs, where its long one-wave
+// chunks stream faster (decode_mma_heads).
 #include "ism_common.h"
 #include "ism_kernels.h"
 
@@ -98,6 +100,7 @@ __device__ __forceinline__ float group_sum(float x) {
 // set hs covers query heads hs GS .. hs GS + GS - 1 of KV head hs GS / G.
 // With G > 8 the G / GS sets of a KV head stream its keys separately.
 // Sets of 4 or more heads go to decode_mma_kernel below, so GS <= 3 here.
+// (Steps with few slabs send every set there.)
 template <int D, int GS, bool PAGED>
 __global__ void __launch_bounds__(256)
 decode_split_kernel(DecodeArgs a) {
@@ -271,7 +274,8 @@ decode_split_kernel(DecodeArgs a) {
 }
 
 // Decode step with matrix cores, for head sets of 4 or more query heads per
-// KV head (the vector kernel above is then bound by its FMAs, not by HBM).
+// KV head (the vector kernel above is then bound by its FMAs, not by HBM),
+// and for sets of any size on steps with few (dialogue, KV head) slabs.
 // One wave per workgroup streams one chunk of one (dialogue, KV head) slab
 // in 32-key tiles through a 2-stage LDS ring (direct global->LDS transfers,
 // the forward kernel's swizzled tile layout) and treats the set's query

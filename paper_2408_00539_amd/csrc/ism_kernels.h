@@ -117,17 +117,25 @@ hipError_t launch_decode(const DecodeArgs &a, int d, hipStream_t stream);
 
 // Decode head sets, with G = hq / hkv query heads per KV head: the
 // matrix-core kernel takes sets of the largest divisor of G up to 32 (the
-// columns of one product) when that is 4 or more; 0 otherwise.
-inline int decode_mma_heads(int hq, int hkv) {
+// columns of one product) when that is 4 or more, or, when the step has
+// fewer than kDecodeVectorSlabs (dialogue, KV head) slabs, of any size;
+// 0 otherwise. Below that slab count its long one-wave chunks stream faster
+// than the vector kernel even for one query head (256 slabs of 8192
+// positions: 6.5 TB/s against 6.2, 6.0 and 5.9 for 1, 2 and 3 heads; 64
+// slabs: 5.6 against 5.2, 4.8 and 4.2); from 1024 slabs on the vector
+// kernel's wider grid is faster for 1-3 heads (6.9, 6.7, 6.7 against 6.4).
+constexpr int kDecodeVectorSlabs = 512;
+inline int decode_mma_heads(int batch, int hq, int hkv) {
   const int g = hq / hkv;
-  for (int s = g < 32 ? g : 32; s >= 4; --s)
+  const int lo = (int64_t)batch * hkv < kDecodeVectorSlabs ? 1 : 4;
+  for (int s = g < 32 ? g : 32; s >= lo; --s)
     if (g % s == 0) return s;
   return 0;
 }
 // Query heads per decode workgroup: the matrix-core set, else (vector kernel,
 // G without a divisor between 4 and 32) the largest divisor of G up to 3.
-inline int decode_heads_per_set(int hq, int hkv) {
-  const int m = decode_mma_heads(hq, hkv);
+inline int decode_heads_per_set(int batch, int hq, int hkv) {
+  const int m = decode_mma_heads(batch, hq, hkv);
   if (m) return m;
   const int g = hq / hkv;
   return g % 3 == 0 ? 3 : g % 2 == 0 ? 2 : 1;

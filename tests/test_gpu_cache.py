@@ -126,22 +126,31 @@ def test_prefill_answer_segment_small(d, hq, hkv):
             compare(f"LSE b{b} q={isq}", lse[:, r0:r1], rl)
 
 
-@pytest.mark.parametrize("hq,hkv", [(4, 4), (16, 2)])
-def test_decode_split_counts_agree(hq, hkv):
+@pytest.mark.parametrize("hq,hkv,B,cap", [(4, 4, 3, 2048), (16, 2, 3, 2048),
+                                           (16, 16, 32, 640), (32, 16, 32, 640),
+                                           (48, 16, 32, 640)])
+def test_decode_split_counts_agree(hq, hkv, B, cap):
     """Any split count merges to the same result (exact merge, R19), for the
-    vector kernel (one query head per KV head) and the matrix-core kernel
-    (8); with 64 splits most chunks of the shorter dialogues are empty."""
+    matrix-core kernel (steps of few (dialogue, KV head) slabs: one and 8
+    query heads per KV head) and the vector kernel (512 slabs: 1, 2 and 3
+    query heads per KV head); with 64 splits most chunks of the shorter
+    dialogues are empty."""
     torch = torch_cuda()
     from paper_2408_00539_amd import ops
-    rng = np.random.default_rng(77)
-    B, d, cap = 3, 128, 2048
+    rng = np.random.default_rng(77 + hq + B)
+    d = 128
     kc = _bits(rng, B, hkv, cap, d)
     vc = _bits(rng, B, hkv, cap, d)
-    pos = np.array([0, 1000, 2047], np.int32)
+    if B == 3:
+        pos = np.array([0, 1000, 2047], np.int32)
+    else:  # chunk and tile edges, the last position, and random ones
+        pos = rng.integers(0, cap, B).astype(np.int32)
+        pos[:6] = [0, 1, 31, 32, 255, 256]
+        pos[-1] = cap - 1
     q, k, v = _bits(rng, B, hq, d), _bits(rng, B, hkv, d), _bits(rng, B, hkv, d)
     outs = []
     for splits in [1, 2, 7, 16, 64]:
-        announce("decode splits", splits)
+        announce("decode splits", hq, hkv, B, splits)
         Kc, Vc = dev_bf16(kc), dev_bf16(vc)
         o, l = ops.decode(dev_bf16(q), dev_bf16(k), dev_bf16(v), Kc, Vc,
                           torch.from_numpy(pos).cuda(), 0, 1 / np.sqrt(d),
