@@ -102,8 +102,15 @@ ism_status hip_status(hipError_t e, const char *what) {
 ism_status validate_segments(const ism_segments *sg, hipStream_t stream) {
   const char *v = getenv("ISM_VALIDATE");
   if (!v || strcmp(v, "1") != 0) return ISM_OK;
-  std::vector<int32_t> cu(sg->batch + 1), cs(sg->num_segs + 1);
-  std::vector<uint8_t> fl(sg->num_segs);
+  std::vector<int32_t> cu, cs;
+  std::vector<uint8_t> fl;
+  try {  // nothing may throw across the C ABI
+    cu.resize(sg->batch + 1);
+    cs.resize(sg->num_segs + 1);
+    fl.resize(sg->num_segs);
+  } catch (...) {
+    return fail(ISM_ERR_SHAPE, "ISM_VALIDATE: no host memory for the segment arrays");
+  }
   hipError_t e = hipStreamSynchronize(stream);
   if (e == hipSuccess)
     e = hipMemcpy(cu.data(), sg->cu_seqlens, cu.size() * 4, hipMemcpyDeviceToHost);
@@ -122,7 +129,12 @@ ism_status validate_new_lengths(const int32_t *cu_new, int32_t batch, int32_t to
                                 int32_t max_new, hipStream_t stream) {
   const char *v = getenv("ISM_VALIDATE");
   if (!v || strcmp(v, "1") != 0) return ISM_OK;
-  std::vector<int32_t> cu(batch + 1);
+  std::vector<int32_t> cu;
+  try {
+    cu.resize(batch + 1);
+  } catch (...) {
+    return fail(ISM_ERR_SHAPE, "ISM_VALIDATE: no host memory for cu_seqlens_new");
+  }
   hipError_t e = hipStreamSynchronize(stream);
   if (e == hipSuccess) e = hipMemcpy(cu.data(), cu_new, cu.size() * 4, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_status(e, "ISM_VALIDATE: copying cu_seqlens_new");
