@@ -4,8 +4,9 @@ dialogues whose segment lengths sit on and around the kernels' tile sizes
 patterns (Eq. 5 for every pattern, R2), head groupings of 1, 2, 3, 4 and 8
 and both head dims, and compares the forward and the backward with the fp64
 oracle; the cache-path tests add groupings of 5, 6, 12 and 16 query heads
-per KV head (the decode's matrix-core sets). Derandomized: the same examples
-run every time."""
+per KV head (the decode's matrix-core sets), and decode steps of 512
+(dialogue, KV head) slabs exercise the vector decode kernel. Derandomized:
+the same examples run every time."""
 
 import numpy as np
 import pytest
@@ -178,3 +179,37 @@ def test_generated_paged_equals_dense(turns, is_query, hh, d, page_size, splits,
                            b.view(torch.int16) if b.dtype == torch.bfloat16 else b)
     for (oa, la), (ob, lb) in zip(outs[2::2], outs[3::2]):
         assert torch.equal(oa.view(torch.int16), ob.view(torch.int16)) and torch.equal(la, lb)
+
+
+@settings(max_examples=20, deadline=None, derandomize=True, database=None)
+@given(pos=st.lists(st.one_of(st.sampled_from([0, 1, 31, 32, 63, 64, 255, 256, 319]),
+                              st.integers(0, 319)), min_size=32, max_size=32),
+       g=st.sampled_from([1, 2, 3]), d=st.sampled_from([64, 128]),
+       splits=st.sampled_from([0, 1, 3, 64]), seed=st.integers(0, 2 ** 31 - 1))
+def test_generated_decode_many_slabs(pos, g, d, splits, seed):
+    """Decode steps of 32 dialogues x 16 KV heads (512 slabs: the vector
+    kernel for 1-3 query heads per KV head) at generated positions, against
+    the oracle's decode step."""
+    torch = torch_cuda()
+    from paper_2408_00539_amd import ops
+    B, hkv, cap = 32, 16, 320
+    hq = g * hkv
+    rng = np.random.default_rng(seed)
+
+    def bits(*shape):
+        return W.to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    kc, vc = bits(B, hkv, cap, d), bits(B, hkv, cap, d)
+    q, kn, vn = bits(B, hq, d), bits(B, hkv, d), bits(B, hkv, d)
+    p = np.array(pos, np.int32)
+    scale = 1 / np.sqrt(d)
+    announce("fuzz decode slabs", g, d, splits, seed)
+    o, lse = ops.decode(dev_bf16(q), dev_bf16(kn), dev_bf16(vn), dev_bf16(kc), dev_bf16(vc),
+                        torch.from_numpy(p).cuda(), 0, scale, num_splits=splits)
+    torch.cuda.synchronize()
+    o, lse = host_f64(o), host_f64(lse)
+    for b in range(B):
+        ro, rl, _, _ = oracle.decode_step(f64(kc[b, :, :p[b]]).transpose(1, 0, 2),
+                                          f64(vc[b, :, :p[b]]).transpose(1, 0, 2),
+                                          f64(q[b]), f64(kn[b]), f64(vn[b]), scale)
+        compare(f"O b{b}", o[b], ro)
+        compare(f"LSE b{b}", lse[:, b], rl)
